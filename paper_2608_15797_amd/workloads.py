@@ -1,0 +1,138 @@
+"""The five synthetic workloads of the candidate-decode hot path, as plain data.
+
+Shapes follow the Qwen2.5-Math models the paper uses (model constants table in
+the overhead-derivation appendix: 7B has 28 layers and 4 KV heads, 72B has 80
+layers and 8 KV heads, the 1.5B helper has 28 layers and 2 KV heads; head_dim
+128 throughout; query heads 28, 64 and 12 come from those models' widths).
+Budgets, windows and buffers follow the eviction settings of the experiment
+setup and implementation-details sections; the detector constants (tau 7.0,
+guard 24, window 12) come from the implementation details. No arithmetic of
+the method lives here.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field, replace
+from typing import Optional
+
+
+@dataclass(frozen=True)
+class BaseShape:
+    """Evicted base-model cache: K,V[S][L][Hkv][cap][D], cap = B + buffer + 1."""
+    S: int
+    L: int
+    Hq: int
+    Hkv: int
+    D: int
+    B: int
+    W: int
+    buffer: int
+    prompt: int
+
+    @property
+    def cap(self) -> int:
+        return self.B + self.buffer + 1
+
+    @property
+    def G(self) -> int:
+        return self.Hq // self.Hkv
+
+
+@dataclass(frozen=True)
+class HelperShape:
+    """Full-context helper: prefix K,V[P][L][Hkv][plen][D] shared by S/P
+    consecutive candidates, plus a private suffix K,V[S][L][Hkv][scap][D]."""
+    S: int
+    L: int
+    Hq: int
+    Hkv: int
+    D: int
+    P: int
+    plen: int
+    scap: int = 512          # at most 512 tokens per reasoning step
+    k_std: float = 1.0       # std of the stored keys
+    scale: Optional[float] = None  # softmax scale; None = 1/sqrt(D)
+
+    @property
+    def G(self) -> int:
+        return self.Hq // self.Hkv
+
+    @property
+    def softmax_scale(self) -> float:
+        return 1.0 / math.sqrt(self.D) if self.scale is None else self.scale
+
+
+@dataclass(frozen=True)
+class LogitSet:
+    R: int
+    V: int
+    std: float
+    n_boost: int = 0
+    boost: float = 0.0
+    near_uniform_frac: float = 0.0
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str                      # "f32" or "bf16"
+    steps: int                      # decode steps after the prompt
+    base: Optional[BaseShape] = None
+    helper: Optional[HelperShape] = None
+    logits: tuple = field(default_factory=tuple)   # LogitSet per model
+    qkv_std: float = 1.0
+    detector: tuple = (12, 24, 7.0)  # (window, guard, tau)
+    seed: int = 0
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+SEED_BASE = 0x4B5652
+
+QWEN7B = dict(L=28, Hq=28, Hkv=4, D=128)
+QWEN72B = dict(L=80, Hq=64, Hkv=8, D=128)
+QWEN15B = dict(L=28, Hq=12, Hkv=2, D=128)
+V_QWEN_BASE = 152064
+V_QWEN_HELPER = 151936
+
+WORKLOADS = {
+    # Tiny oracle case: 1 sequence, GQA 4:1, head_dim 64, fp32, B=16, window 8,
+    # buffer 16, prompt 32 then 64 decode steps, logits V=1024 ~ N(0, 2^2).
+    "tiny": Workload(
+        name="tiny", dtype="f32", steps=64,
+        base=BaseShape(S=1, L=1, Hq=4, Hkv=1, D=64, B=16, W=8, buffer=16, prompt=32),
+        logits=(LogitSet(R=1, V=1024, std=2.0),), seed=SEED_BASE + 1),
+    # Helper-only full-context decode (1.5B shape): 8 private contexts of 4096,
+    # keys stored pre-scaled by 1/sqrt(128) and attended with scale 1.
+    "helper4k": Workload(
+        name="helper4k", dtype="bf16", steps=512,
+        helper=HelperShape(S=8, P=8, plen=4096, k_std=1.0 / math.sqrt(128), scale=1.0,
+                           **QWEN15B),
+        logits=(LogitSet(R=8, V=V_QWEN_HELPER, std=3.0, n_boost=5, boost=10.0),),
+        seed=SEED_BASE + 2),
+    # Evicted 7B decode: 16 problems x 4 candidates, B=128, window 32, buffer 128.
+    "base7b": Workload(
+        name="base7b", dtype="bf16", steps=1024,
+        base=BaseShape(S=64, B=128, W=32, buffer=128, prompt=256, **QWEN7B),
+        logits=(LogitSet(R=64, V=V_QWEN_BASE, std=3.0, n_boost=5, boost=10.0),),
+        seed=SEED_BASE + 3),
+    # 7B at B=64 with 16 x 8 candidates, plus the 1.5B helper over 16 shared
+    # 8192-token contexts (one per problem, 8 candidates each).
+    "base7b_helper": Workload(
+        name="base7b_helper", dtype="bf16", steps=4096,
+        base=BaseShape(S=128, B=64, W=32, buffer=64, prompt=256, **QWEN7B),
+        helper=HelperShape(S=128, P=16, plen=8192, **QWEN15B),
+        logits=(LogitSet(R=128, V=V_QWEN_BASE, std=1.0),
+                LogitSet(R=128, V=V_QWEN_HELPER, std=1.0)),
+        seed=SEED_BASE + 4),
+    # 72B at B=64 with 8 x 4 candidates, plus the helper over 32 private
+    # 16384-token contexts; 5% of logit rows near-uniform.
+    "base72b_helper": Workload(
+        name="base72b_helper", dtype="bf16", steps=8192,
+        base=BaseShape(S=32, B=64, W=32, buffer=64, prompt=256, **QWEN72B),
+        helper=HelperShape(S=32, P=32, plen=16384, **QWEN15B),
+        logits=(LogitSet(R=32, V=V_QWEN_BASE, std=3.0, n_boost=5, boost=10.0,
+                         near_uniform_frac=0.05),),
+        seed=SEED_BASE + 5),
+}

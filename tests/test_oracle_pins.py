@@ -1,0 +1,342 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each test checks the oracle against something other than itself: brute force
+on tiny inputs, a library routine (torch's scaled_dot_product_attention,
+scipy's entropy), a closed form, or an invariant the method guarantees.
+No GPU is used.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.run import BaseOracle, window_start
+
+rng = np.random.default_rng(1234)
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    return torch.from_numpy(np.asarray(x, np.float32)).to(torch.bfloat16).view(torch.int16) \
+        .numpy().view(np.uint16)
+
+
+def bf16_value(bits: np.ndarray) -> np.ndarray:
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+
+
+def sdpa_gqa(q, K, V, n, scale):
+    """Library attention: torch SDPA in fp64, KV heads repeated for GQA.
+    q[L][Hq][D], K,V[L][Hkv][cap][D] (float64) -> [L][Hq][D]."""
+    L, Hq, D = q.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    Kr = torch.from_numpy(K[:, :, :n]).repeat_interleave(G, dim=1)
+    Vr = torch.from_numpy(V[:, :, :n]).repeat_interleave(G, dim=1)
+    qt = torch.from_numpy(q)[:, :, None, :]
+    o = torch.nn.functional.scaled_dot_product_attention(qt, Kr, Vr, scale=scale)
+    return o[:, :, 0, :].numpy()
+
+
+# ---------------------------------------------------------------- P7: library
+
+@pytest.mark.parametrize("Hq,Hkv,D,n", [(4, 1, 64, 1), (4, 1, 64, 33), (28, 4, 128, 97),
+                                        (12, 2, 128, 130), (6, 6, 32, 17)])
+def test_attention_matches_torch_sdpa(Hq, Hkv, D, n):
+    """Eq. (1) attention equals softmax(scale q K^T) V from torch (GQA mapping
+    qh -> qh // G, softmax scale, masking of slots beyond n)."""
+    S, L, cap = 2, 3, n + 5
+    K = rng.standard_normal((S, L, Hkv, cap, D)).astype(np.float32)
+    V = rng.standard_normal((S, L, Hkv, cap, D)).astype(np.float32)
+    K[:, :, :, n:] = 1e4  # stale slots must not matter
+    V[:, :, :, n:] = np.nan
+    q = rng.standard_normal((S, L, Hq, D)).astype(np.float32)
+    scale = 1 / math.sqrt(D)
+    out, psum = oracle.decode_attn(K, V, n, q, scale)
+    for s in range(S):
+        ref = sdpa_gqa(q[s].astype(np.float64), K[s].astype(np.float64),
+                       V[s].astype(np.float64), n, scale)
+        np.testing.assert_allclose(out[s], ref, rtol=1e-12, atol=1e-12)
+    # P3: each query row's probabilities sum to one, so each KV head collects G.
+    np.testing.assert_allclose(psum.sum(-1), Hq // Hkv, rtol=1e-12)
+    assert (psum[..., n:] == 0).all()
+
+
+def test_attention_bf16_inputs_decoded_exactly():
+    """bf16 inputs are widened bit-exactly: same result as fp64 attention on the
+    bf16-rounded values."""
+    S, L, Hkv, Hq, D, n = 1, 2, 2, 12, 128, 40
+    Kf = rng.standard_normal((S, L, Hkv, n, D)).astype(np.float32)
+    Vf = rng.standard_normal((S, L, Hkv, n, D)).astype(np.float32)
+    qf = rng.standard_normal((S, L, Hq, D)).astype(np.float32)
+    K, V, q = bf16_bits(Kf), bf16_bits(Vf), bf16_bits(qf)
+    out, _ = oracle.decode_attn(K, V, n, q, 0.125)
+    ref = sdpa_gqa(bf16_value(q[0]), bf16_value(K[0]), bf16_value(V[0]), n, 0.125)
+    np.testing.assert_allclose(out[0], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_prefix_attention_is_attention_over_concatenation():
+    """Helper path (Eq. (3) full context): prefix then own cache equals one
+    attention over the concatenated keys (torch SDPA)."""
+    S, P, L, Hkv, Hq, D, plen, n = 4, 2, 2, 2, 12, 64, 50, 7
+    PK = rng.standard_normal((P, L, Hkv, plen, D)).astype(np.float32)
+    PV = rng.standard_normal((P, L, Hkv, plen, D)).astype(np.float32)
+    K = rng.standard_normal((S, L, Hkv, 16, D)).astype(np.float32)
+    V = rng.standard_normal((S, L, Hkv, 16, D)).astype(np.float32)
+    q = rng.standard_normal((S, L, Hq, D)).astype(np.float32)
+    out, _ = oracle.decode_attn(K, V, n, q, 0.1, prefix_K=PK, prefix_V=PV)
+    for s in range(S):
+        p = s // (S // P)
+        Kc = np.concatenate([PK[p], K[s]], axis=2).astype(np.float64)
+        Vc = np.concatenate([PV[p], V[s]], axis=2).astype(np.float64)
+        ref = sdpa_gqa(q[s].astype(np.float64), Kc, Vc, plen + n, 0.1)
+        np.testing.assert_allclose(out[s], ref, rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------- P6: special cases
+
+def test_attention_special_cases():
+    S, L, Hkv, Hq, D, cap = 1, 1, 2, 8, 16, 9
+    K = rng.standard_normal((S, L, Hkv, cap, D)).astype(np.float32)
+    V = rng.standard_normal((S, L, Hkv, cap, D)).astype(np.float32)
+    q = rng.standard_normal((S, L, Hq, D)).astype(np.float32)
+    G = Hq // Hkv
+    # n = 1: the only value comes back unchanged.
+    out, _ = oracle.decode_attn(K, V, 1, q, 0.3)
+    for qh in range(Hq):
+        np.testing.assert_array_equal(out[0, 0, qh], V[0, 0, qh // G, 0].astype(np.float64))
+    # scale 0: uniform weights, the mean of the values.
+    out, psum = oracle.decode_attn(K, V, 6, q, 0.0)
+    for qh in range(Hq):
+        np.testing.assert_allclose(out[0, 0, qh], V[0, 0, qh // G, :6].astype(np.float64).mean(0), rtol=1e-12,
+                                   atol=1e-14)
+    np.testing.assert_allclose(psum[0, 0, :, :6], G / 6, rtol=1e-12)
+    # identical keys: also uniform.
+    K2 = K.copy()
+    K2[:, :, :, :] = K[:, :, :, :1]
+    out, _ = oracle.decode_attn(K2, V, 5, q, 0.7)
+    for qh in range(Hq):
+        np.testing.assert_allclose(out[0, 0, qh], V[0, 0, qh // G, :5].astype(np.float64).mean(0), rtol=1e-12,
+                                   atol=1e-14)
+    # identical query across the group: the head's mass is G x one head's.
+    q2 = q.copy()
+    for h in range(Hkv):
+        q2[0, 0, h * G:(h + 1) * G] = q[0, 0, h * G]
+    _, ps_group = oracle.decode_attn(K, V, 7, q2, 0.5)
+    _, ps_single = oracle.decode_attn(K[:, :, :1], V[:, :, :1], 7, q2[:, :, :1], 0.5)
+    np.testing.assert_allclose(ps_group[0, 0, 0], G * ps_single[0, 0, 0], rtol=1e-12)
+
+
+# ------------------------------------------------------------- P1: brute force
+
+def _separated_scores(m):
+    """Distinct scores with pairwise gaps >= 1e-3 in random order."""
+    base = np.arange(m) * 2e-3 + rng.uniform(0, 5e-4, m)
+    return rng.permutation(base) + 0.3
+
+
+@pytest.mark.parametrize("n,B,W", [(9, 5, 2), (12, 6, 3), (16, 8, 4), (14, 7, 1), (10, 10, 3),
+                                   (11, 4, 3)])
+def test_topb_matches_brute_force_subset(n, B, W):
+    """TopB of Eq. (1): the kept non-window subset is the (B-W)-subset with the
+    largest total score, found by enumerating every subset; the W newest slots
+    are always kept."""
+    for _ in range(5):
+        sc = _separated_scores(n)
+        kept = oracle.select_topb(sc, n, B, W)
+        best = max(itertools.combinations(range(n - W), B - W), key=lambda c: sc[list(c)].sum())
+        assert list(kept) == sorted(best) + list(range(n - W, n))
+
+
+def test_topb_tie_break_lower_slot_and_full_sort():
+    """Ties go to the lower slot; result equals a stable full sort by
+    (score desc, slot asc)."""
+    for _ in range(50):
+        n = int(rng.integers(6, 40))
+        W = int(rng.integers(1, 5))
+        B = int(rng.integers(W + 1, n + 1))
+        sc = rng.integers(0, 4, n).astype(np.float64)  # many exact ties
+        kept = oracle.select_topb(sc, n, B, W)
+        order = sorted(range(n - W), key=lambda j: (-sc[j], j))[: B - W]
+        assert list(kept) == sorted(order) + list(range(n - W, n))
+
+
+# ---------------------------------------------------- P3, P4, P8: the full loop
+
+def _tiny_run(seed=7, S=2, L=2, Hkv=2, Hq=4, D=16, B=8, W=3, buffer=4, T=40, record_pre=True):
+    orc = BaseOracle(S, L, Hkv, Hq, D, B, W, buffer, np.float32, 1 / math.sqrt(D),
+                     record_pre=record_pre)
+    g = np.random.default_rng(seed)
+    toks = [(g.standard_normal((S, L, Hq, D)).astype(np.float32),
+             g.standard_normal((S, L, Hkv, D)).astype(np.float32),
+             g.standard_normal((S, L, Hkv, D)).astype(np.float32)) for _ in range(T)]
+    outs = [orc.step(t, *toks[t]) for t in range(T)]
+    return orc, toks, outs
+
+
+def test_eviction_invariants():
+    """P3 + P4: at every eviction the scores sum to W*G (W window rows of
+    probabilities, G query heads per KV head); the kept set has exactly B
+    entries, includes the W newest positions, keeps temporal order, and the
+    compacted rows are bitwise the source rows."""
+    B, W, buffer, G = 8, 3, 4, 2
+    orc, toks, _ = _tiny_run(B=B, W=W, buffer=buffer)
+    assert len(orc.events) == 6  # n: 13 at t=12, then every buffer+1 = 5 tokens
+    assert [e["t"] for e in orc.events] == [12, 17, 22, 27, 32, 37]
+    for e in orc.events:
+        np.testing.assert_allclose(e["score"].sum(-1), W * G, rtol=1e-12)
+        kp = e["kept_pos"]
+        assert kp.shape[-1] == B
+        assert (np.diff(kp, axis=-1) > 0).all()
+        assert (kp[..., -W:] == np.arange(e["t"] - W + 1, e["t"] + 1)).all()
+        Kpre, Vpre, _ = e["pre"]
+        kept = e["kept"]
+        src = np.take_along_axis(Kpre, kept[..., None], axis=3)
+        # state right after this eviction is reproduced by replaying: check via
+        # the recorded pre-state of the next event (rows < B untouched until then
+        # only for rows that survive); direct check on the final state below.
+    last = orc.events[-1]
+    Kpre, Vpre, ppre = last["pre"]
+    # Tokens appended after the last eviction occupy slots B..n-1; slots < B hold
+    # exactly the kept rows, bit for bit.
+    for arr, pre in ((orc.K, Kpre), (orc.V, Vpre)):
+        src = np.take_along_axis(pre, last["kept"][..., None], axis=3)
+        assert np.array_equal(arr[:, :, :, :B].view(np.uint32), src.view(np.uint32))
+    assert np.array_equal(orc.pos[:, :, :, :B], last["kept_pos"])
+
+
+def test_no_eviction_equals_full_attention():
+    """When B is at least the context length nothing is evicted and the
+    evicted-cache attention equals full attention over the whole history
+    (torch SDPA over all tokens so far)."""
+    S, L, Hkv, Hq, D, T = 1, 2, 2, 6, 32, 30
+    orc = BaseOracle(S, L, Hkv, Hq, D, T + 5, 4, 4, np.float32, 0.2)
+    g = np.random.default_rng(3)
+    Ks, Vs = [], []
+    for t in range(T):
+        q = g.standard_normal((S, L, Hq, D)).astype(np.float32)
+        k = g.standard_normal((S, L, Hkv, D)).astype(np.float32)
+        v = g.standard_normal((S, L, Hkv, D)).astype(np.float32)
+        Ks.append(k)
+        Vs.append(v)
+        out = orc.step(t, q, k, v)
+        Kh = np.stack(Ks, axis=3)[0].astype(np.float64)
+        Vh = np.stack(Vs, axis=3)[0].astype(np.float64)
+        ref = sdpa_gqa(q[0].astype(np.float64), Kh, Vh, t + 1, 0.2)
+        np.testing.assert_allclose(out[0], ref, rtol=1e-12, atol=1e-12)
+    assert orc.events == []
+
+
+def test_streaming_scores_equal_window_recompute():
+    """P8: the score summed step by step over the window equals a single causal
+    re-computation from the W window queries against the pre-eviction cache."""
+    B, W, buffer = 8, 3, 4
+    orc, toks, _ = _tiny_run(B=B, W=W, buffer=buffer)
+    for e in orc.events:
+        t, n = e["t"], e["n"]
+        Kpre, Vpre, _ = e["pre"]
+        q_win = np.stack([toks[t - (W - 1 - r)][0] for r in range(W)], axis=3)
+        sc = oracle.window_scores(Kpre, Vpre, n, q_win, orc.scale)
+        np.testing.assert_allclose(sc[..., :n], e["score"], rtol=1e-12, atol=1e-15)
+        assert (sc[..., n:] == 0).all()
+
+
+def test_window_rows_pad_later_slots_with_zero():
+    """A window step of length n gives no mass to slots >= n: the first window
+    row's contribution to the newest slot is zero."""
+    B, W, buffer = 8, 3, 4
+    orc, toks, _ = _tiny_run(B=B, W=W, buffer=buffer, T=13)
+    e = orc.events[0]
+    n = e["n"]
+    assert n == B + buffer + 1 and window_start(B, W, buffer) == n - W + 1
+    Kpre, Vpre, _ = e["pre"]
+    # Only the newest query sees the newest slot.
+    q_last = toks[e["t"]][0]
+    _, ps = oracle.decode_attn(Kpre, Vpre, n, q_last, orc.scale)
+    np.testing.assert_allclose(e["score"][..., n - 1], ps[..., n - 1], rtol=1e-12)
+
+
+# ------------------------------------------------------------- P5: entropy
+
+@pytest.mark.parametrize("V", [1, 2, 7, 1024, 152064])
+def test_entropy_uniform_is_log_v(V):
+    H = oracle.entropy(np.full((2, V), 0.37, np.float32))
+    np.testing.assert_allclose(H, math.log(V), rtol=1e-10, atol=1e-12)
+
+
+def test_entropy_one_hot_and_single():
+    x = np.full((3, 50), -np.inf, np.float32)
+    x[0, 3] = 1.0
+    x[1, 49] = -5.0
+    x[2, 0] = 0.0
+    np.testing.assert_array_equal(oracle.entropy(x), 0.0)
+    np.testing.assert_array_equal(oracle.entropy(np.array([[4.2]], np.float32)), 0.0)
+
+
+@pytest.mark.parametrize("V,k,a,b", [(10, 3, 2.0, -1.0), (152064, 5, 10.0, 0.0),
+                                     (1000, 999, 0.0, 3.0)])
+def test_entropy_two_level_closed_form(V, k, a, b):
+    """k logits at a, V-k at b. With d = a - b and Z = k e^d + (V-k):
+    H = ln Z - k d e^d / Z."""
+    x = np.full((1, V), b, np.float64)
+    x[0, :k] = a
+    d = a - b
+    Z = k * math.exp(d) + (V - k)
+    ref = math.log(Z) - k * d * math.exp(d) / Z
+    np.testing.assert_allclose(oracle.entropy(x.astype(np.float32)), ref, rtol=1e-10)
+
+
+def test_entropy_matches_scipy_and_invariances():
+    from scipy.special import softmax
+    from scipy.stats import entropy
+    x = (rng.standard_normal((4, 3000)) * 3).astype(np.float32)
+    H = oracle.entropy(x)
+    ref = entropy(softmax(x.astype(np.float64), axis=1), axis=1)
+    np.testing.assert_allclose(H, ref, rtol=1e-10)
+    np.testing.assert_allclose(oracle.entropy(x + np.float32(5.0)), H, rtol=1e-6)
+    np.testing.assert_allclose(oracle.entropy(x[:, rng.permutation(3000)]), H, rtol=1e-10)
+    # inv_temp scales logits before the softmax.
+    ref_t = entropy(softmax(1.25 * x.astype(np.float64), axis=1), axis=1)
+    np.testing.assert_allclose(oracle.entropy(x, inv_temp=1.25), ref_t, rtol=1e-10)
+
+
+def test_entropy_bf16_and_ld():
+    xf = (rng.standard_normal((3, 500)) * 2).astype(np.float32)
+    xb = bf16_bits(xf)
+    padded = np.zeros((3, 512), np.uint16)
+    padded[:, :500] = xb
+    padded[:, 500:] = bf16_bits(np.full((3, 12), 50.0, np.float32))  # must be ignored
+    from scipy.special import softmax
+    from scipy.stats import entropy
+    ref = entropy(softmax(bf16_value(xb), axis=1), axis=1)
+    np.testing.assert_allclose(oracle.entropy(padded, V=500), ref, rtol=1e-10)
+
+
+# ------------------------------------------------------------- detector
+
+def test_detector_fires_exactly_at_guard_for_sustained_high_entropy():
+    """Eq. (4) moving average with guard 24 and window 12, tau 7.0: uniform
+    rows over 2048 tokens (H = ln 2048 = 7.62) fire at the 24th token, not
+    before; confident rows (H ~ 0) never fire."""
+    R = 3
+    det = oracle.Detector(R, window=12, guard=24, tau=7.0)
+    hi = oracle.entropy(np.zeros((1, 2048), np.float32))[0]
+    lo = 0.0
+    for pos in range(1, 40):
+        H = np.array([hi, lo, hi if pos > 30 else lo])
+        flag = det.step(H)
+        assert flag[0] == (1 if pos >= 24 else 0)
+        assert flag[1] == 0
+        # row 2: high from position 31 on; the mean of 12 exceeds 7 once
+        # k high values satisfy k * 7.62 / 12 > 7, i.e. k >= 12 -> position 42.
+        assert flag[2] == 0
+
+
+def test_detector_mean_is_over_last_window():
+    det = oracle.Detector(1, window=4, guard=4, tau=2.0)
+    seq = [0, 0, 0, 0, 9, 0, 0, 0, 3, 3, 3]
+    flags = [int(det.step(np.array([h]))[0]) for h in seq]
+    # means of the last 4: pos4 0, pos5 2.25 -> fires and stays set.
+    assert flags == [0, 0, 0, 0, 1, 1, 1, 1, 1, 1, 1]
