@@ -1,0 +1,219 @@
+/*
+ * kvr.h -- C ABI of the KV-Rescue candidate-decode hot path (arxiv 2608.15797)
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The library computes, for a batch of candidate sequences decoding one token
+ * each (Eq. (3): N base and N helper candidates are sampled per reasoning step
+ * and decoded together):
+ *   - grouped-query decode attention over a KV-evicted cache (Eq. (1), third
+ *     line) or over a full-context cache made of a shared prefix plus a private
+ *     suffix (the full-context helper of Sec. 3.1), with the new token's key
+ *     and value appended in the same call;
+ *   - the accumulated-attention importance score of Sec. 2.1, summed over an
+ *     observation window, either streamed during decode or recomputed from the
+ *     window's queries;
+ *   - TopB selection with a protected recent window and in-place compaction of
+ *     every KV head (Eq. (1), first two lines; eviction settings of Sec. 4.1
+ *     and the implementation details);
+ *   - the full-vocabulary token entropy of Eq. (4) with the moving-average
+ *     degeneration detector of Sec. 3.2.
+ *
+ * Conventions shared by every entry point
+ *   - All array pointers are DEVICE pointers owned by the caller. The library
+ *     never allocates, frees or retains them, and keeps no global state: calls
+ *     on different streams are independent when their buffers do not alias.
+ *   - Arrays are row-major with the innermost index last. Element types are
+ *     float32 (KVR_F32) or bfloat16 (KVR_BF16); arithmetic is float32.
+ *   - bfloat16 arrays and float32 vector arrays must be 16-byte aligned.
+ *   - Every call validates its arguments on the host and returns a status;
+ *     on any error nothing is enqueued. Work is enqueued on `stream` (NULL =
+ *     the default stream) and completes asynchronously; a device fault shows
+ *     up at the caller's next synchronisation.
+ *   - Live lengths (len[s]) are caller-owned device arrays the library only
+ *     reads; the caller advances them (a decode driver knows every length in
+ *     advance: +1 per token, B after an eviction).
+ */
+#ifndef KVR_H
+#define KVR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define KVR_OK 0
+#define KVR_EINVAL (-1)        /* bad pointer, shape, alignment or policy     */
+#define KVR_EUNSUPPORTED (-2)  /* valid but not implemented (dtype, D, G, LDS) */
+#define KVR_EHIP (-3)          /* the HIP runtime refused a launch            */
+#define KVR_EWORKSPACE (-4)    /* workspace missing or too small              */
+
+/* Element types. */
+#define KVR_F32 0
+#define KVR_BF16 1
+
+/* Static description of a per-sequence KV cache.
+ *   k, v : [S][L][Hkv][cap][D] elements of `dtype`, device memory.
+ *   pos  : [S][L][Hkv][cap] int32 original token position of each slot, or
+ *          NULL when positions are not tracked. */
+typedef struct kvr_cache {
+    void *k;
+    void *v;
+    int32_t *pos;
+    int32_t S, L, Hkv, cap, D;
+    int32_t dtype;
+} kvr_cache;
+
+/* Full-context prefix shared by groups of candidates (Sec. 2.2: candidates of
+ * one step share the committed context).
+ *   k, v : [P][L][Hkv][plen][D] of the cache dtype. Sequence s reads prefix
+ *          s / (S / P); S must be a multiple of P (P == S: private contexts). */
+typedef struct kvr_prefix {
+    const void *k;
+    const void *v;
+    int32_t P, plen;
+} kvr_prefix;
+
+/* Eviction policy (Eq. (1) TopB with a protected recent window).
+ *   B      : entries kept after an eviction, including the window;
+ *   W      : protected recent window, also the observation window whose
+ *            attention mass forms the importance score; 0 < W < B;
+ *   buffer : headroom; a sequence evicts when its live length exceeds
+ *            B + buffer. buffer >= W - 1 so every window step follows the
+ *            previous eviction. The cache needs cap >= B + buffer + 1. */
+typedef struct kvr_policy {
+    int32_t B, W, buffer;
+} kvr_policy;
+
+/* Entropy-detector state for R candidate rows (Eq. (4) moving average;
+ * implementation details: tau = 7.0, guard 24, window 12).
+ *   hist : [R][window] float32, last `window` entropies in push order mod window;
+ *   cnt  : [R] int32, entropies pushed so far;
+ *   flag : [R] uint8, sticky degeneration flag.
+ * State starts zeroed. Each call pushes H[r], increments cnt[r] and, once
+ * cnt[r] >= guard, sets flag[r] = 1 if the mean of the last min(cnt, window)
+ * entropies exceeds tau. */
+typedef struct kvr_detector {
+    float *hist;
+    int32_t *cnt;
+    uint8_t *flag;
+    int32_t window, guard;
+    float tau;
+} kvr_detector;
+
+/* Message for a status code (static storage). */
+const char *kvr_strerror(int status);
+
+/* Human-readable detail of the last failing call on this host thread. */
+const char *kvr_last_error(void);
+
+/*
+ * kvr_decode_attn -- one decode step of grouped-query attention for S
+ * candidate sequences and all L layers (Eq. (1) third line; Eq. (3)).
+ *
+ *   cache   : the sequences' own caches (evicted base cache, or the helper's
+ *             private suffix). Written only at slot len[s]-1 (append).
+ *   prefix  : NULL, or the shared full-context prefix attended before the own
+ *             cache (helper). Requires a workspace (see below).
+ *   len     : [S] int32 device, live entries of sequence s INCLUDING the token
+ *             appended by this call; 1 <= len[s] <= cap.
+ *   q       : [S][L][Hq][D], Hq = G * Hkv, 1 <= G <= 16. Query head qh reads
+ *             KV head qh / G.
+ *   scale   : softmax scale applied to q.k (commonly 1/sqrt(D)).
+ *   k_new, v_new : [S][L][Hkv][D] key/value of the new token, written to slot
+ *             len[s]-1 before attending; NULL when the caller already stored
+ *             them (then both must be NULL).
+ *   new_pos : [S] int32 original position of the new token, stored into
+ *             cache->pos when both are non-NULL.
+ *   out     : [S][L][Hq][D] attention output, cache dtype.
+ *   policy, scores : NULL/NULL for no scoring. Otherwise scores is
+ *             [S][L][Hkv][cap] float32 and the call streams the importance
+ *             score: a sequence whose len n satisfies n >= B + buffer + 2 - W
+ *             is in its observation window; for such a sequence, with
+ *             r_j = sum over the G query heads of KV head h of softmax
+ *             probability of slot j, the call sets scores[j] = r_j when n is
+ *             the first window length or j == n-1, and scores[j] += r_j
+ *             otherwise, for j < n. Other sequences' scores are untouched.
+ *             Scoring is not available together with a prefix.
+ *   workspace, workspace_bytes : device scratch of at least
+ *             kvr_decode_attn_workspace_size() bytes (no initialisation
+ *             needed); may be NULL/0 when that size is 0.
+ * Errors: KVR_EINVAL (shape, pointer, alignment, policy), KVR_EUNSUPPORTED
+ * (D not 64/128, G > 16, dtype, LDS limit), KVR_EWORKSPACE, KVR_EHIP.
+ */
+int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len,
+                    const void *q, int32_t Hq, float scale, const void *k_new,
+                    const void *v_new, const int32_t *new_pos, void *out,
+                    const kvr_policy *policy, float *scores, void *workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes kvr_decode_attn needs for this geometry (0 without prefix). */
+size_t kvr_decode_attn_workspace_size(const kvr_cache *cache, const kvr_prefix *prefix,
+                                      int32_t Hq);
+
+/*
+ * kvr_accumulate_scores -- importance score recomputed from the last nq
+ * queries of every sequence (accumulated attention of Sec. 2.1 over an
+ * observation window; used when a step's tokens are encoded in one pass, as
+ * when a helper step is committed to the base, Sec. 3.1 and Alg. 1).
+ *
+ *   cache, len : as for kvr_decode_attn (len includes all nq window tokens,
+ *             which must already be in the cache).
+ *   q_win   : [S][L][Hq][nq][D] queries of the last nq tokens, oldest first.
+ *             Window row r attends causally over len[s] - (nq-1-r) entries.
+ *   scores  : [S][L][Hkv][cap] float32. For j < len[s]: scores[j] = sum over
+ *             rows r and the G query heads of KV head h of the probability of
+ *             slot j (0 where row r cannot see j). accumulate != 0 adds to the
+ *             stored value instead of overwriting. Slots >= len[s] untouched.
+ */
+int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void *q_win,
+                          int32_t nq, int32_t Hq, float scale, float *scores,
+                          int32_t accumulate, hipStream_t stream);
+
+/*
+ * kvr_evict_topb -- TopB eviction with a protected recent window and in-place
+ * compaction (Eq. (1) first two lines).
+ *
+ * For every sequence with n = len[s] > B + buffer, and every (layer, KV head)
+ * independently: the W newest slots [n-W, n) are kept; of the slots [0, n-W)
+ * the B-W with the largest scores are kept, ties going to the lower slot. The
+ * kept rows of k, v (and pos) move to slots 0..B-1 in their original order.
+ * Sequences with len[s] <= B + buffer are not touched. The caller sets the new
+ * live length B for evicted sequences.
+ *
+ *   scores : [S][L][Hkv][cap] float32 importance scores (read only).
+ *   kept   : NULL or [S][L][Hkv][B] int32, receives the kept pre-eviction slot
+ *            ids in ascending order for evicted sequences.
+ */
+int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scores,
+                   const kvr_policy *policy, int32_t *kept, hipStream_t stream);
+
+/*
+ * kvr_logit_entropy -- token entropy H = -sum_v p(v) log p(v) of
+ * p = softmax(inv_temp * logits) for R rows (Eq. (4)), natural log.
+ *
+ *   logits : [R][ld] of `dtype`; the first V columns of each row are used.
+ *            ld >= V; for 16-byte vector loads ld * element size should be a
+ *            multiple of 16 (other ld values run a scalar path).
+ *   H      : [R] float32 output.
+ *   det    : NULL, or detector state updated with the new entropies.
+ *   workspace : at least kvr_logit_entropy_workspace_size(R, V) bytes, zero
+ *            filled before its first use; every completed call leaves it
+ *            zeroed again. May be NULL/0 when that size is 0.
+ * -inf logits are allowed (they contribute 0); a row of only -inf is invalid.
+ */
+int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,
+                      float inv_temp, float *H, const kvr_detector *det, void *workspace,
+                      size_t workspace_bytes, hipStream_t stream);
+
+size_t kvr_logit_entropy_workspace_size(int32_t R, int32_t V);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVR_H */

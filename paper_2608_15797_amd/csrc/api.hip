@@ -1,0 +1,216 @@
+// C ABI of libkvr: argument validation and dispatch to the gfx950 kernels.
+// Every entry point checks its arguments on the host before enqueuing
+// anything; on error it returns a status and records a message retrievable
+// with kvr_last_error() on the same thread.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "../../include/kvr.h"
+#include "kvr_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int hip_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return KVR_OK;
+  return fail(KVR_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Shared checks of a cache description; sets G when Hq > 0.
+int check_cache(const kvr_cache *c, int32_t Hq, int *G, bool need_pos_ok = true) {
+  (void)need_pos_ok;
+  if (!c) return fail(KVR_EINVAL, "cache is NULL");
+  if (!c->k || !c->v) return fail(KVR_EINVAL, "cache k/v pointer is NULL");
+  if (c->S <= 0 || c->L <= 0 || c->Hkv <= 0 || c->cap <= 0 || c->D <= 0)
+    return fail(KVR_EINVAL, "cache dims must be positive (S=%d L=%d Hkv=%d cap=%d D=%d)", c->S,
+                c->L, c->Hkv, c->cap, c->D);
+  if (c->dtype != KVR_F32 && c->dtype != KVR_BF16)
+    return fail(KVR_EUNSUPPORTED, "dtype %d is not KVR_F32 or KVR_BF16", c->dtype);
+  if (c->D != 64 && c->D != 128) return fail(KVR_EUNSUPPORTED, "head_dim %d is not 64 or 128", c->D);
+  if (!aligned16(c->k) || !aligned16(c->v)) return fail(KVR_EINVAL, "cache k/v not 16-byte aligned");
+  if ((double)c->S * c->L * c->Hkv > 2147483647.0)
+    return fail(KVR_EUNSUPPORTED, "S*L*Hkv exceeds the launch grid");
+  if (Hq > 0) {
+    if (Hq % c->Hkv != 0) return fail(KVR_EINVAL, "Hq=%d is not a multiple of Hkv=%d", Hq, c->Hkv);
+    *G = Hq / c->Hkv;
+    if (*G > 16) return fail(KVR_EUNSUPPORTED, "G=%d query heads per KV head exceeds 16", *G);
+  }
+  return KVR_OK;
+}
+
+int check_policy(const kvr_policy *pol, int cap) {
+  if (pol->W <= 0 || pol->W >= pol->B)
+    return fail(KVR_EINVAL, "policy needs 0 < W < B (B=%d W=%d)", pol->B, pol->W);
+  if (pol->buffer < pol->W - 1)
+    return fail(KVR_EINVAL, "policy needs buffer >= W-1 (buffer=%d W=%d)", pol->buffer, pol->W);
+  if ((long)pol->B + pol->buffer + 1 > cap)
+    return fail(KVR_EINVAL, "cap=%d < B+buffer+1=%ld", cap, (long)pol->B + pol->buffer + 1);
+  return KVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *kvr_strerror(int status) {
+  switch (status) {
+    case KVR_OK: return "ok";
+    case KVR_EINVAL: return "invalid argument";
+    case KVR_EUNSUPPORTED: return "unsupported configuration";
+    case KVR_EHIP: return "HIP runtime error";
+    case KVR_EWORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+  }
+}
+
+const char *kvr_last_error(void) { return g_err; }
+
+size_t kvr_decode_attn_workspace_size(const kvr_cache *cache, const kvr_prefix *prefix, int32_t Hq) {
+  if (!cache || !prefix || prefix->P <= 0 || cache->dtype != KVR_BF16) return 0;
+  int ns = 1, ch = 64;
+  kvr::plan_prefix_splits(prefix->P, cache->L, cache->Hkv, prefix->plen, &ns, &ch);
+  return kvr::attn_workspace_bytes(cache->S, cache->L, Hq, cache->D, ns);
+}
+
+int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len,
+                    const void *q, int32_t Hq, float scale, const void *k_new, const void *v_new,
+                    const int32_t *new_pos, void *out, const kvr_policy *policy, float *scores,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  int G = 0;
+  int st = check_cache(cache, Hq, &G);
+  if (st) return st;
+  if (Hq <= 0) return fail(KVR_EINVAL, "Hq must be positive");
+  if (!len || !q || !out) return fail(KVR_EINVAL, "len, q and out are required");
+  if (!aligned16(q) || !aligned16(out)) return fail(KVR_EINVAL, "q/out not 16-byte aligned");
+  if ((k_new == nullptr) != (v_new == nullptr))
+    return fail(KVR_EINVAL, "k_new and v_new must both be given or both be NULL");
+  if (k_new && (!aligned16(k_new) || !aligned16(v_new)))
+    return fail(KVR_EINVAL, "k_new/v_new not 16-byte aligned");
+  if ((policy == nullptr) != (scores == nullptr))
+    return fail(KVR_EINVAL, "policy and scores must both be given or both be NULL");
+  kvr::AttnParams p{};
+  p.k = cache->k; p.v = cache->v; p.pos = cache->pos;
+  p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.Hq = Hq; p.G = G;
+  p.cap = cache->cap; p.D = cache->D; p.dtype = cache->dtype;
+  p.len = len; p.q = q; p.k_new = k_new; p.v_new = v_new; p.new_pos = new_pos; p.out = out;
+  p.scale = scale;
+  if (policy) {
+    st = check_policy(policy, cache->cap);
+    if (st) return st;
+    if (prefix && prefix->P > 0) return fail(KVR_EINVAL, "scoring is not available with a prefix");
+    if (!aligned16(scores)) return fail(KVR_EINVAL, "scores not 16-byte aligned");
+    p.scores = scores; p.B = policy->B; p.W = policy->W; p.buffer = policy->buffer;
+    if (cache->dtype == KVR_BF16) {
+      const size_t lds = ((size_t)G * ((cache->cap + 63) & ~63) + 32) * sizeof(float);
+      if (lds > 65536) return fail(KVR_EUNSUPPORTED, "scoring needs %zu bytes of LDS (> 64 KiB)", lds);
+    }
+  }
+  if (prefix && prefix->P > 0) {
+    if (!prefix->k || !prefix->v) return fail(KVR_EINVAL, "prefix k/v pointer is NULL");
+    if (prefix->plen <= 0) return fail(KVR_EINVAL, "prefix plen must be positive");
+    if (cache->S % prefix->P != 0)
+      return fail(KVR_EINVAL, "S=%d is not a multiple of the prefix count P=%d", cache->S, prefix->P);
+    if (!aligned16(prefix->k) || !aligned16(prefix->v))
+      return fail(KVR_EINVAL, "prefix k/v not 16-byte aligned");
+    p.pk = prefix->k; p.pv = prefix->v; p.P = prefix->P; p.plen = prefix->plen;
+    p.C = cache->S / prefix->P;
+    if (cache->dtype == KVR_BF16) {
+      if (p.C * G > 64)
+        return fail(KVR_EUNSUPPORTED, "%d candidates x %d heads per shared prefix exceeds 64 rows", p.C, G);
+      kvr::plan_prefix_splits(p.P, p.L, p.Hkv, p.plen, &p.nsplit, &p.chunk);
+      const size_t need = kvr::attn_workspace_bytes(p.S, p.L, Hq, p.D, p.nsplit);
+      if (!workspace || workspace_bytes < need)
+        return fail(KVR_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+      if (!aligned16(workspace)) return fail(KVR_EINVAL, "workspace not 16-byte aligned");
+      p.ws = static_cast<float *>(workspace);
+    }
+  }
+  if (cache->dtype == KVR_F32) {
+    const size_t nt = (size_t)(p.P > 0 ? p.plen : 0) + p.cap;
+    const size_t lds = ((size_t)G * p.D + (size_t)G * nt + 32) * sizeof(float);
+    if (lds > 65536) return fail(KVR_EUNSUPPORTED, "float32 path needs %zu bytes of LDS (> 64 KiB)", lds);
+  }
+  return hip_status(kvr::launch_decode_attn(p, stream), "kvr_decode_attn launch");
+}
+
+int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void *q_win,
+                          int32_t nq, int32_t Hq, float scale, float *scores, int32_t accumulate,
+                          hipStream_t stream) {
+  int G = 0;
+  int st = check_cache(cache, Hq, &G);
+  if (st) return st;
+  if (Hq <= 0 || nq <= 0) return fail(KVR_EINVAL, "Hq and nq must be positive");
+  if (!len || !q_win || !scores) return fail(KVR_EINVAL, "len, q_win and scores are required");
+  const size_t lds = ((size_t)cache->D + 2 * (size_t)cache->cap) * sizeof(float);
+  if (lds > 65536) return fail(KVR_EUNSUPPORTED, "cap=%d needs too much LDS", cache->cap);
+  kvr::ScoreParams p{};
+  p.k = cache->k; p.v = cache->v;
+  p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.Hq = Hq; p.G = G;
+  p.cap = cache->cap; p.D = cache->D; p.dtype = cache->dtype;
+  p.len = len; p.q_win = q_win; p.nq = nq; p.scale = scale; p.scores = scores;
+  p.accumulate = accumulate != 0;
+  return hip_status(kvr::launch_accumulate_scores(p, stream), "kvr_accumulate_scores launch");
+}
+
+int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scores,
+                   const kvr_policy *policy, int32_t *kept, hipStream_t stream) {
+  int G = 0;
+  int st = check_cache(cache, 0, &G);
+  if (st) return st;
+  if (!len || !scores || !policy) return fail(KVR_EINVAL, "len, scores and policy are required");
+  st = check_policy(policy, cache->cap);
+  if (st) return st;
+  const size_t lds = (size_t)(2 * cache->cap + policy->B) * sizeof(uint32_t);
+  if (lds > 65536) return fail(KVR_EUNSUPPORTED, "cap=%d needs too much LDS", cache->cap);
+  kvr::EvictParams p{};
+  p.k = cache->k; p.v = cache->v; p.pos = cache->pos;
+  p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.cap = cache->cap; p.D = cache->D;
+  p.dtype = cache->dtype; p.len = len; p.scores = scores;
+  p.B = policy->B; p.W = policy->W; p.buffer = policy->buffer; p.kept = kept;
+  return hip_status(kvr::launch_evict_topb(p, stream), "kvr_evict_topb launch");
+}
+
+size_t kvr_logit_entropy_workspace_size(int32_t R, int32_t V) {
+  if (R <= 0 || V <= 0) return 0;
+  return kvr::entropy_workspace_bytes(R, V);
+}
+
+int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,
+                      float inv_temp, float *H, const kvr_detector *det, void *workspace,
+                      size_t workspace_bytes, hipStream_t stream) {
+  if (!logits || !H) return fail(KVR_EINVAL, "logits and H are required");
+  if (dtype != KVR_F32 && dtype != KVR_BF16) return fail(KVR_EUNSUPPORTED, "dtype %d", dtype);
+  if (R <= 0 || V <= 0 || ld < V) return fail(KVR_EINVAL, "need R > 0, V > 0, ld >= V (R=%d V=%d ld=%ld)", R, V, (long)ld);
+  if (R > 65535) return fail(KVR_EUNSUPPORTED, "R=%d rows exceeds 65535", R);
+  kvr::EntropyParams p{};
+  p.logits = logits; p.dtype = dtype; p.R = R; p.V = V; p.ld = ld; p.inv_temp = inv_temp; p.H = H;
+  if (det) {
+    if (!det->hist || !det->cnt || !det->flag) return fail(KVR_EINVAL, "detector arrays are required");
+    if (det->window <= 0 || det->guard < 0) return fail(KVR_EINVAL, "detector window must be positive");
+    p.hist = det->hist; p.cnt = det->cnt; p.flag = det->flag;
+    p.window = det->window; p.guard = det->guard; p.tau = det->tau;
+  }
+  p.splits = kvr::entropy_splits(R, V);
+  const size_t need = kvr::entropy_workspace_bytes(R, V);
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need)
+      return fail(KVR_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+    if (!aligned16(workspace)) return fail(KVR_EINVAL, "workspace not 16-byte aligned");
+    p.ws = workspace;
+  }
+  return hip_status(kvr::launch_logit_entropy(p, stream), "kvr_logit_entropy launch");
+}
+
+}  // extern "C"

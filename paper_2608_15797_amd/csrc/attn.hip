@@ -1,0 +1,609 @@
+// Grouped-query decode attention for KV-Rescue candidate batches on gfx950.
+//
+// Computes, per candidate s, layer l and query head qh (KV head h = qh / G),
+// o = sum_j softmax_j(scale * q.k_j) v_j over the sequence's live cache
+// entries (Eq. (1), third line), optionally preceded by a shared full-context
+// prefix (the helper of Sec. 3.1), and streams the per-KV-head attention mass
+// that forms the accumulated-attention importance score (Sec. 2.1).
+//
+// bf16 path: one 64-lane wave per (sequence, layer, KV head) unit. The G query
+// heads of a KV head form the 16 rows of an MFMA tile, so q.K^T and P.V are
+// 16x16x16 bf16 matrix-core products:
+//   * S^T = K . Q^T : A = 16 keys x 16 d (each lane loads 16 contiguous bytes of
+//     one key row), B = Q^T held in registers for the whole unit. The output
+//     layout (lane = query row + 16 * key group) is exactly the A-operand
+//     layout P needs for P . V, so probabilities never leave registers.
+//   * O = P . V : B = 16 keys x 16 d. Each lane loads 16 contiguous bytes of
+//     four consecutive key rows (fully coalesced: 4 rows x 256 B per load
+//     instruction) and transposes 4x8 bf16 in registers with bit operations,
+//     which assigns output column n to d = n * (D/16) + b for instance b.
+// The softmax is online over chunks of 64 keys with running max and sum kept
+// in the log2 domain. Logits of window steps go to LDS so the normalised
+// probabilities can be summed over the G heads after the last chunk.
+//
+// Helper (prefix) path: split-K over the prefix; one wave per
+// (prefix, layer, KV head, split) processes the query rows of all candidates
+// sharing the prefix (up to 4 row blocks = 64 rows), so shared context is
+// read from HBM once per step. The private suffix runs as its own unit. Both
+// write (max, sum, unnormalised o) partials, merged by log-sum-exp.
+//
+// f32 path: plain VALU kernel (one wave per unit) for float32 caches.
+#include <hip/hip_runtime.h>
+
+#include "kvr_device.h"
+#include "kvr_internal.h"
+
+namespace kvr {
+
+namespace {
+
+constexpr float kNegInf = -__builtin_huge_valf();
+
+template <int D>
+struct Geo {
+  static constexpr int NB = D / 16;   // MFMA instances per 16-key tile
+  static constexpr int NLD = D / 32;  // 16-byte loads per lane per K row
+  static constexpr int VW = NB / 2;   // 32-bit words per lane per V row
+};
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ short4_t s4(uint32_t a, uint32_t b) {
+  u32x2 v = {a, b};
+  return __builtin_bit_cast(short4_t, v);
+}
+
+__device__ __forceinline__ float4_t mfma16(short4_t a, short4_t b, float4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+// Q^T operands of one query row (or zeros). d(g, b, c) = (b/2)*32 + g*8 + (b%2)*4 + c.
+template <int D>
+__device__ __forceinline__ void load_qop(const bf16_t *qrow, int g4, short4_t (&qop)[Geo<D>::NB]) {
+#pragma unroll
+  for (int i = 0; i < Geo<D>::NLD; i++) {
+    u32x4 w = {0u, 0u, 0u, 0u};
+    if (qrow) w = *reinterpret_cast<const u32x4 *>(qrow + i * 32 + g4 * 8);
+    qop[2 * i] = s4(w.x, w.y);
+    qop[2 * i + 1] = s4(w.z, w.w);
+  }
+}
+
+// K operands of one key row with the same d mapping as load_qop.
+template <int D>
+__device__ __forceinline__ void load_krow(const bf16_t *krow, int g4, u32x4 (&w)[Geo<D>::NLD]) {
+#pragma unroll
+  for (int i = 0; i < Geo<D>::NLD; i++) {
+    if (krow)
+      w[i] = *reinterpret_cast<const u32x4 *>(krow + i * 32 + g4 * 8);
+    else
+      w[i] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// The lane's part of one V row: D/16 elements at n * (D/16).
+template <int D>
+__device__ __forceinline__ void load_vrow(const bf16_t *vrow, int r16, uint32_t (&w)[Geo<D>::VW]) {
+  if constexpr (D == 128) {
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (vrow) x = *reinterpret_cast<const u32x4 *>(vrow + r16 * 8);
+    w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w;
+  } else {
+    u32x2 x = {0u, 0u};
+    if (vrow) x = *reinterpret_cast<const u32x2 *>(vrow + r16 * 4);
+    w[0] = x.x; w[1] = x.y;
+  }
+}
+
+// B operand of P.V instance b from four V rows (keys 4*g4 + c, c = 0..3).
+template <int D>
+__device__ __forceinline__ short4_t vop(const uint32_t (&v)[4][Geo<D>::VW], int b) {
+  const int w = b >> 1;
+  if ((b & 1) == 0)
+    return s4((v[0][w] & 0xffffu) | (v[1][w] << 16), (v[2][w] & 0xffffu) | (v[3][w] << 16));
+  return s4((v[0][w] >> 16) | (v[1][w] & 0xffff0000u), (v[2][w] >> 16) | (v[3][w] & 0xffff0000u));
+}
+
+__device__ __forceinline__ short4_t pop4(float a, float b, float c, float d) {
+  return s4(pack_bf16x2(a, b), pack_bf16x2(c, d));
+}
+
+// Online-softmax state of the lane's query row within one 16-row block.
+struct RowState {
+  float m;   // running max of logits (log2 domain)
+  float zl;  // lane-local partial sum of exp2(x - m)
+};
+
+// Process one chunk of TILES*16 keys for one row block. x[t][i] are the
+// lane's logits (log2 domain, masked = -inf). Updates state, rescales o and
+// accumulates P.V with the chunk's V rows.
+template <int D, int TILES>
+__device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st,
+                                           float4_t (&o)[Geo<D>::NB],
+                                           const uint32_t (&vr)[TILES][4][Geo<D>::VW], int g4) {
+  float cm = kNegInf;
+#pragma unroll
+  for (int t = 0; t < TILES; t++)
+#pragma unroll
+    for (int i = 0; i < 4; i++) cm = fmaxf(cm, x[t][i]);
+  cm = fmaxf(cm, shfl_xor(cm, 16));
+  cm = fmaxf(cm, shfl_xor(cm, 32));
+  const float mn = fmaxf(st.m, cm);
+  const bool live = mn != kNegInf;
+  const float alpha = live ? fast_exp2(st.m - mn) : 1.0f;
+  float psum = 0.0f;
+#pragma unroll
+  for (int t = 0; t < TILES; t++)
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      x[t][i] = live ? fast_exp2(x[t][i] - mn) : 0.0f;
+      psum += x[t][i];
+    }
+  st.zl = st.zl * alpha + psum;
+  st.m = mn;
+  // o rows are 4*g4 + i; their alphas live in lanes 4*g4 + i.
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const float ai = __shfl(alpha, 4 * g4 + i, kWave);
+#pragma unroll
+    for (int b = 0; b < Geo<D>::NB; b++) o[b][i] *= ai;
+  }
+#pragma unroll
+  for (int t = 0; t < TILES; t++) {
+    const short4_t pa = pop4(x[t][0], x[t][1], x[t][2], x[t][3]);
+#pragma unroll
+    for (int b = 0; b < Geo<D>::NB; b++) o[b] = mfma16(pa, vop<D>(vr[t], b), o[b]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Own-cache kernel: base (evicted cache, optional score streaming) or helper
+// suffix (PARTIAL: writes a log-sum-exp partial into split slot nsplit).
+template <int D, bool PARTIAL>
+__global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
+  constexpr int TILES = 4;
+  constexpr int NB = Geo<D>::NB;
+  extern __shared__ float smem[];
+
+  const int unit = blockIdx.x;  // ((s * L) + l) * Hkv + h
+  const int h = unit % p.Hkv;
+  const int sl = unit / p.Hkv;
+  const int l = sl % p.L;
+  const int s = sl / p.L;
+  const int lane = threadIdx.x;
+  const int r16 = lane & 15;
+  const int g4 = lane >> 4;
+  const int G = p.G;
+
+  int n = p.len[s];
+  n = n < 0 ? 0 : (n > p.cap ? p.cap : n);
+  const size_t ubase = (size_t)unit * p.cap * D;
+  bf16_t *Kc = static_cast<bf16_t *>(p.k) + ubase;
+  bf16_t *Vc = static_cast<bf16_t *>(p.v) + ubase;
+  const bf16_t *kn = p.k_new ? static_cast<const bf16_t *>(p.k_new) + (size_t)unit * D : nullptr;
+  const bf16_t *vn = p.v_new ? static_cast<const bf16_t *>(p.v_new) + (size_t)unit * D : nullptr;
+
+  // Append the new token at slot n-1 (reads below take it from k_new/v_new).
+  if (kn && n >= 1) {
+    constexpr int LPR = D / 8;  // lanes per row, 16 bytes each
+    if (lane < LPR) {
+      reinterpret_cast<u32x4 *>(Kc + (size_t)(n - 1) * D)[lane] = reinterpret_cast<const u32x4 *>(kn)[lane];
+    } else if (lane < 2 * LPR) {
+      const int i = lane - LPR;
+      reinterpret_cast<u32x4 *>(Vc + (size_t)(n - 1) * D)[i] = reinterpret_cast<const u32x4 *>(vn)[i];
+    } else if (lane == 2 * LPR && p.pos && p.new_pos) {
+      p.pos[(size_t)unit * p.cap + n - 1] = p.new_pos[s];
+    }
+  }
+
+  const int qh0 = h * G;
+  const size_t qrow0 = ((size_t)s * p.L + l) * p.Hq + qh0;
+  short4_t qop[NB];
+  load_qop<D>(r16 < G ? static_cast<const bf16_t *>(p.q) + (qrow0 + r16) * D : nullptr, g4, qop);
+
+  // Observation-window step of this sequence?
+  const int wstart = p.B + p.buffer + 2 - p.W;
+  const bool win = !PARTIAL && p.scores != nullptr && n >= wstart;
+  const int ldx = (p.cap + 63) & ~63;
+  float *xs = smem;                 // [G][ldx] logits of window steps
+  float *stat = smem + G * ldx;     // [16] max, [16] 1/sum
+
+  const float sl2 = p.scale * kLog2e;
+  RowState st{kNegInf, 0.0f};
+  float4_t o[NB];
+#pragma unroll
+  for (int b = 0; b < NB; b++) o[b] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int c0 = 0; c0 < n; c0 += 16 * TILES) {
+    u32x4 kr[TILES][Geo<D>::NLD];
+    uint32_t vr[TILES][4][Geo<D>::VW];
+#pragma unroll
+    for (int t = 0; t < TILES; t++) {
+      const int key = c0 + t * 16 + r16;
+      const bf16_t *krow = key < n ? ((kn && key == n - 1) ? kn : Kc + (size_t)key * D) : nullptr;
+      load_krow<D>(krow, g4, kr[t]);
+    }
+#pragma unroll
+    for (int t = 0; t < TILES; t++)
+#pragma unroll
+      for (int c = 0; c < 4; c++) {
+        const int key = c0 + t * 16 + 4 * g4 + c;
+        const bf16_t *vrow = key < n ? ((vn && key == n - 1) ? vn : Vc + (size_t)key * D) : nullptr;
+        load_vrow<D>(vrow, r16, vr[t][c]);
+      }
+    float x[TILES][4];
+#pragma unroll
+    for (int t = 0; t < TILES; t++) {
+      float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < Geo<D>::NLD; i++) {
+        acc = mfma16(s4(kr[t][i].x, kr[t][i].y), qop[2 * i], acc);
+        acc = mfma16(s4(kr[t][i].z, kr[t][i].w), qop[2 * i + 1], acc);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int key = c0 + t * 16 + 4 * g4 + i;
+        x[t][i] = key < n ? acc[i] * sl2 : kNegInf;
+      }
+      if (win && r16 < G)
+        *reinterpret_cast<float4_t *>(xs + r16 * ldx + c0 + t * 16 + 4 * g4) =
+            float4_t{x[t][0], x[t][1], x[t][2], x[t][3]};
+    }
+    softmax_pv<D, TILES>(x, st, o, vr, g4);
+  }
+
+  float z = st.zl;
+  z += shfl_xor(z, 16);
+  z += shfl_xor(z, 32);
+
+  if constexpr (PARTIAL) {
+    float *ws = p.ws;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int row = 4 * g4 + i;
+      const float mi = __shfl(st.m, row, kWave);
+      const float zi = __shfl(z, row, kWave);
+      if (row < G) {
+        const size_t rec = (((size_t)p.nsplit * p.S + s) * p.L + l) * p.Hq + qh0 + row;
+        float *r = ws + rec * (D + 4);
+        if (r16 == 0) { r[0] = mi; r[1] = zi; }
+#pragma unroll
+        for (int b = 0; b < NB; b++) r[4 + r16 * NB + b] = o[b][i];
+      }
+    }
+  } else {
+    bf16_t *out = static_cast<bf16_t *>(p.out);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int row = 4 * g4 + i;
+      const float zi = __shfl(z, row, kWave);
+      if (row < G) {
+        const float inv = 1.0f / zi;
+        uint32_t w[NB / 2];
+#pragma unroll
+        for (int b = 0; b < NB / 2; b++) w[b] = pack_bf16x2(o[2 * b][i] * inv, o[2 * b + 1][i] * inv);
+        bf16_t *dst = out + (qrow0 + row) * D + r16 * NB;
+        if constexpr (D == 128)
+          *reinterpret_cast<u32x4 *>(dst) = u32x4{w[0], w[1], w[2], w[3]};
+        else
+          *reinterpret_cast<u32x2 *>(dst) = u32x2{w[0], w[1]};
+      }
+    }
+    if (win) {
+      if (g4 == 0 && r16 < G) {
+        stat[r16] = st.m;
+        stat[16 + r16] = 1.0f / z;
+      }
+      __syncthreads();
+      const bool first = n == wstart;
+      float *sc = p.scores + (size_t)unit * p.cap;
+      for (int j = lane; j < n; j += kWave) {
+        float r = 0.0f;
+        for (int g = 0; g < G; g++) r += fast_exp2(xs[g * ldx + j] - stat[g]) * stat[16 + g];
+        if (first || j == n - 1)
+          sc[j] = r;
+        else
+          sc[j] += r;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Prefix kernel: one wave per (prefix, layer, KV head, split); RB row blocks
+// of 16 rows hold the C*G query rows (candidate c, head g) sharing the prefix.
+template <int D, int RB>
+__global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
+  constexpr int TILES = RB == 1 ? 4 : 2;
+  constexpr int NB = Geo<D>::NB;
+  const int nunits = p.P * p.L * p.Hkv;
+  const int split = blockIdx.x / nunits;
+  const int unit = blockIdx.x % nunits;  // ((pp * L) + l) * Hkv + h
+  const int h = unit % p.Hkv;
+  const int pl = unit / p.Hkv;
+  const int l = pl % p.L;
+  const int pp = pl / p.L;
+  const int lane = threadIdx.x;
+  const int r16 = lane & 15;
+  const int g4 = lane >> 4;
+  const int G = p.G;
+  const int rows = p.C * G;
+
+  const bf16_t *Kp = static_cast<const bf16_t *>(p.pk) + (size_t)unit * p.plen * D;
+  const bf16_t *Vp = static_cast<const bf16_t *>(p.pv) + (size_t)unit * p.plen * D;
+  const int k0 = split * p.chunk;
+  const int k1 = min(k0 + p.chunk, p.plen);
+
+  short4_t qop[RB][NB];
+#pragma unroll
+  for (int rb = 0; rb < RB; rb++) {
+    const int rho = rb * 16 + r16;
+    const bf16_t *qrow = nullptr;
+    if (rho < rows) {
+      const int c = rho / G, g = rho % G;
+      const int s = pp * p.C + c;
+      qrow = static_cast<const bf16_t *>(p.q) + (((size_t)s * p.L + l) * p.Hq + h * G + g) * D;
+    }
+    load_qop<D>(qrow, g4, qop[rb]);
+  }
+
+  const float sl2 = p.scale * kLog2e;
+  RowState st[RB];
+  float4_t o[RB][NB];
+#pragma unroll
+  for (int rb = 0; rb < RB; rb++) {
+    st[rb] = RowState{kNegInf, 0.0f};
+#pragma unroll
+    for (int b = 0; b < NB; b++) o[rb][b] = float4_t{0.f, 0.f, 0.f, 0.f};
+  }
+
+  for (int c0 = k0; c0 < k1; c0 += 16 * TILES) {
+    u32x4 kr[TILES][Geo<D>::NLD];
+    uint32_t vr[TILES][4][Geo<D>::VW];
+#pragma unroll
+    for (int t = 0; t < TILES; t++) {
+      const int key = c0 + t * 16 + r16;
+      load_krow<D>(key < k1 ? Kp + (size_t)key * D : nullptr, g4, kr[t]);
+    }
+#pragma unroll
+    for (int t = 0; t < TILES; t++)
+#pragma unroll
+      for (int c = 0; c < 4; c++) {
+        const int key = c0 + t * 16 + 4 * g4 + c;
+        load_vrow<D>(key < k1 ? Vp + (size_t)key * D : nullptr, r16, vr[t][c]);
+      }
+#pragma unroll
+    for (int rb = 0; rb < RB; rb++) {
+      float x[TILES][4];
+#pragma unroll
+      for (int t = 0; t < TILES; t++) {
+        float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < Geo<D>::NLD; i++) {
+          acc = mfma16(s4(kr[t][i].x, kr[t][i].y), qop[rb][2 * i], acc);
+          acc = mfma16(s4(kr[t][i].z, kr[t][i].w), qop[rb][2 * i + 1], acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+          const int key = c0 + t * 16 + 4 * g4 + i;
+          x[t][i] = key < k1 ? acc[i] * sl2 : kNegInf;
+        }
+      }
+      softmax_pv<D, TILES>(x, st[rb], o[rb], vr, g4);
+    }
+  }
+
+  float *ws = p.ws;
+#pragma unroll
+  for (int rb = 0; rb < RB; rb++) {
+    float z = st[rb].zl;
+    z += shfl_xor(z, 16);
+    z += shfl_xor(z, 32);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int rl = 4 * g4 + i;
+      const float mi = __shfl(st[rb].m, rl, kWave);
+      const float zi = __shfl(z, rl, kWave);
+      const int rho = rb * 16 + rl;
+      if (rho < rows) {
+        const int c = rho / G, g = rho % G;
+        const int s = pp * p.C + c;
+        const size_t rec = (((size_t)split * p.S + s) * p.L + l) * p.Hq + h * G + g;
+        float *r = ws + rec * (D + 4);
+        if (r16 == 0) { r[0] = mi; r[1] = zi; }
+#pragma unroll
+        for (int b = 0; b < NB; b++) r[4 + r16 * NB + b] = o[rb][b][i];
+      }
+    }
+  }
+}
+
+// Log-sum-exp merge of nsplit + 1 partials per query row; one wave per row.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_bf16(AttnParams p) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int nrows = p.S * p.L * p.Hq;
+  if (row >= nrows) return;
+  const int nparts = p.nsplit + 1;
+  const size_t stride = (size_t)nrows * (D + 4);
+  const float *base = p.ws + (size_t)row * (D + 4);
+  float M = kNegInf;
+  for (int k = 0; k < nparts; k++) M = fmaxf(M, base[k * stride]);
+  constexpr int PER = D / 64;
+  float acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; e++) acc[e] = 0.f;
+  float Z = 0.f;
+  for (int k = 0; k < nparts; k++) {
+    const float *r = base + k * stride;
+    const float w = r[0] == kNegInf ? 0.f : fast_exp2(r[0] - M);
+    Z += r[1] * w;
+    // record layout: o element for lane-of-origin n, instance b at 4 + n*NB + b,
+    // i.e. d = n*NB + b maps to record index 4 + d.
+#pragma unroll
+    for (int e = 0; e < PER; e++) acc[e] += r[4 + lane * PER + e] * w;
+  }
+  const float inv = 1.0f / Z;
+  bf16_t *out = static_cast<bf16_t *>(p.out) + (size_t)row * D + lane * PER;
+  if constexpr (PER == 2)
+    *reinterpret_cast<uint32_t *>(out) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  else
+    out[0] = (bf16_t)f32_to_bf16_bits(acc[0] * inv);
+}
+
+// ---------------------------------------------------------------------------
+// float32 path: one wave per (sequence, layer, KV head), VALU arithmetic.
+// LDS: q rows [G][D], logits [G][nt_max], stats [2][16].
+__global__ __launch_bounds__(64) void attn_f32(AttnParams p, int nt_max) {
+  extern __shared__ float smem[];
+  const int unit = blockIdx.x;
+  const int h = unit % p.Hkv;
+  const int sl = unit / p.Hkv;
+  const int l = sl % p.L;
+  const int s = sl / p.L;
+  const int lane = threadIdx.x;
+  const int G = p.G, D = p.D;
+  int n = p.len[s];
+  n = n < 0 ? 0 : (n > p.cap ? p.cap : n);
+  const int npre = p.P > 0 ? p.plen : 0;
+  const int nt = npre + n;
+  const size_t ubase = (size_t)unit * p.cap * D;
+  float *Kc = static_cast<float *>(p.k) + ubase;
+  float *Vc = static_cast<float *>(p.v) + ubase;
+  const float *kn = p.k_new ? static_cast<const float *>(p.k_new) + (size_t)unit * D : nullptr;
+  const float *vn = p.v_new ? static_cast<const float *>(p.v_new) + (size_t)unit * D : nullptr;
+  const float *Kp = nullptr, *Vp = nullptr;
+  if (p.P > 0) {
+    const int pp = s / p.C;
+    const size_t pbase = (((size_t)pp * p.L + l) * p.Hkv + h) * (size_t)p.plen * D;
+    Kp = static_cast<const float *>(p.pk) + pbase;
+    Vp = static_cast<const float *>(p.pv) + pbase;
+  }
+  if (kn && n >= 1) {
+    for (int d = lane; d < D; d += kWave) {
+      Kc[(size_t)(n - 1) * D + d] = kn[d];
+      Vc[(size_t)(n - 1) * D + d] = vn[d];
+    }
+    if (lane == 0 && p.pos && p.new_pos) p.pos[(size_t)unit * p.cap + n - 1] = p.new_pos[s];
+  }
+  auto krow = [&](int j) -> const float * {
+    if (j < npre) return Kp + (size_t)j * D;
+    const int js = j - npre;
+    return (kn && js == n - 1) ? kn : Kc + (size_t)js * D;
+  };
+  auto vrow = [&](int j) -> const float * {
+    if (j < npre) return Vp + (size_t)j * D;
+    const int js = j - npre;
+    return (vn && js == n - 1) ? vn : Vc + (size_t)js * D;
+  };
+  float *qs = smem;
+  float *xs = smem + G * D;
+  float *stat = xs + (size_t)G * nt_max;
+  const size_t qrow0 = ((size_t)s * p.L + l) * p.Hq + h * G;
+  for (int e = lane; e < G * D; e += kWave) qs[e] = static_cast<const float *>(p.q)[qrow0 * D + e];
+  __syncthreads();
+  for (int g = 0; g < G; g++) {
+    float mloc = kNegInf;
+    for (int j = lane; j < nt; j += kWave) {
+      const float *kr = krow(j);
+      float dot = 0.f;
+      for (int d = 0; d < D; d++) dot = fmaf(qs[g * D + d], kr[d], dot);
+      const float x = dot * p.scale;
+      xs[g * nt_max + j] = x;
+      mloc = fmaxf(mloc, x);
+    }
+    const float m = wave_max(mloc);
+    float zloc = 0.f;
+    for (int j = lane; j < nt; j += kWave) zloc += expf(xs[g * nt_max + j] - m);
+    const float z = wave_sum(zloc);
+    if (lane == 0) { stat[g] = m; stat[16 + g] = 1.0f / z; }
+  }
+  __syncthreads();
+  float *out = static_cast<float *>(p.out);
+  for (int g = 0; g < G; g++) {
+    const float m = stat[g], iz = stat[16 + g];
+    for (int d = lane; d < D; d += kWave) {
+      float acc = 0.f;
+      for (int j = 0; j < nt; j++) acc = fmaf(expf(xs[g * nt_max + j] - m) * iz, vrow(j)[d], acc);
+      out[(qrow0 + g) * D + d] = acc;
+    }
+  }
+  const int wstart = p.B + p.buffer + 2 - p.W;
+  if (p.scores != nullptr && p.P == 0 && n >= wstart) {
+    const bool first = n == wstart;
+    float *sc = p.scores + (size_t)unit * p.cap;
+    for (int j = lane; j < n; j += kWave) {
+      float r = 0.f;
+      for (int g = 0; g < G; g++) r += expf(xs[g * nt_max + j] - stat[g]) * stat[16 + g];
+      if (first || j == n - 1)
+        sc[j] = r;
+      else
+        sc[j] += r;
+    }
+  }
+}
+
+template <int D>
+hipError_t launch_bf16(const AttnParams &p, hipStream_t stream) {
+  if (p.P == 0) {
+    const size_t lds = p.scores ? ((size_t)p.G * ((p.cap + 63) & ~63) + 32) * sizeof(float) : 0;
+    hipLaunchKernelGGL((attn_cache_bf16<D, false>), dim3(p.S * p.L * p.Hkv), dim3(64), lds, stream, p);
+    return hipGetLastError();
+  }
+  const int rb = (p.C * p.G + 15) / 16;
+  const dim3 gridA(p.P * p.L * p.Hkv * p.nsplit);
+  switch (rb) {
+    case 1: hipLaunchKernelGGL((attn_prefix_bf16<D, 1>), gridA, dim3(64), 0, stream, p); break;
+    case 2: hipLaunchKernelGGL((attn_prefix_bf16<D, 2>), gridA, dim3(64), 0, stream, p); break;
+    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3>), gridA, dim3(64), 0, stream, p); break;
+    case 4: hipLaunchKernelGGL((attn_prefix_bf16<D, 4>), gridA, dim3(64), 0, stream, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_cache_bf16<D, true>), dim3(p.S * p.L * p.Hkv), dim3(64), 0, stream, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nrows = p.S * p.L * p.Hq;
+  hipLaunchKernelGGL((attn_merge_bf16<D>), dim3((nrows + 3) / 4), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t f32_attn_lds_bytes(int G, int D, int plen, int cap) {
+  return ((size_t)G * D + (size_t)G * (plen + cap) + 32) * sizeof(float);
+}
+
+void plan_prefix_splits(int P, int L, int Hkv, int plen, int *nsplit, int *chunk) {
+  // Aim for >= 2048 waves over the prefix, with chunks of at least 512 keys
+  // (multiples of 64 so every chunk but the last is whole tiles).
+  const long units = (long)P * L * Hkv;
+  long ns = (2048 + units - 1) / units;
+  const long maxs = (plen + 511) / 512;
+  if (ns > maxs) ns = maxs;
+  if (ns < 1) ns = 1;
+  long ch = (plen + ns - 1) / ns;
+  ch = (ch + 63) / 64 * 64;
+  ns = (plen + ch - 1) / ch;
+  *nsplit = (int)(ns < 1 ? 1 : ns);
+  *chunk = (int)(ch < 64 ? 64 : ch);
+}
+
+size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit) {
+  return (size_t)(nsplit + 1) * S * L * Hq * (D + 4) * sizeof(float);
+}
+
+hipError_t launch_decode_attn(const AttnParams &p, hipStream_t stream) {
+  if (p.dtype == 0) {
+    const int nt_max = (p.P > 0 ? p.plen : 0) + p.cap;
+    const size_t lds = f32_attn_lds_bytes(p.G, p.D, p.P > 0 ? p.plen : 0, p.cap);
+    hipLaunchKernelGGL(attn_f32, dim3(p.S * p.L * p.Hkv), dim3(64), lds, stream, p, nt_max);
+    return hipGetLastError();
+  }
+  return p.D == 128 ? launch_bf16<128>(p, stream) : launch_bf16<64>(p, stream);
+}
+
+}  // namespace kvr

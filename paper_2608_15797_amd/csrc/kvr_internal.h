@@ -1,0 +1,82 @@
+// Host-side interface between the C ABI layer (api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kvr {
+
+// Geometry and pointers of one kvr_decode_attn call, after validation.
+struct AttnParams {
+  // own cache [S][L][Hkv][cap][D], pos [S][L][Hkv][cap]
+  void *k, *v;
+  int32_t *pos;
+  int S, L, Hkv, Hq, G, cap, D;
+  int dtype;
+  // prefix [P][L][Hkv][plen][D]; P == 0 without prefix
+  const void *pk, *pv;
+  int P, plen, C;  // C = S / P candidates per prefix
+  const int32_t *len;
+  const void *q;
+  const void *k_new, *v_new;
+  const int32_t *new_pos;
+  void *out;
+  float scale;
+  // scoring (scores == nullptr: off)
+  float *scores;
+  int B, W, buffer;
+  // split-K partials for the prefix path: ws [nsplit+1][S][L][Hq][D+4] floats
+  float *ws;
+  int nsplit, chunk;
+};
+
+// Split plan for the prefix path; identical on the size query and the call.
+void plan_prefix_splits(int P, int L, int Hkv, int plen, int *nsplit, int *chunk);
+size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit);
+
+hipError_t launch_decode_attn(const AttnParams &p, hipStream_t stream);
+
+struct ScoreParams {
+  const void *k, *v;
+  int S, L, Hkv, Hq, G, cap, D, dtype;
+  const int32_t *len;
+  const void *q_win;
+  int nq;
+  float scale;
+  float *scores;
+  int accumulate;
+};
+hipError_t launch_accumulate_scores(const ScoreParams &p, hipStream_t stream);
+
+struct EvictParams {
+  void *k, *v;
+  int32_t *pos;
+  int S, L, Hkv, cap, D, dtype;
+  const int32_t *len;
+  const float *scores;
+  int B, W, buffer;
+  int32_t *kept;
+};
+hipError_t launch_evict_topb(const EvictParams &p, hipStream_t stream);
+
+struct EntropyParams {
+  const void *logits;
+  int dtype;
+  int R, V;
+  int64_t ld;
+  float inv_temp;
+  float *H;
+  float *hist;
+  int32_t *cnt;
+  uint8_t *flag;
+  int window, guard;
+  float tau;
+  void *ws;
+  int splits;
+};
+int entropy_splits(int R, int V);
+size_t entropy_workspace_bytes(int R, int V);
+hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream);
+
+}  // namespace kvr

@@ -1,0 +1,87 @@
+"""The C-ABI library loads on the host, exports every function include/kvr.h
+declares, and rejects bad arguments on the host before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "kvr.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvr_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_four_entry_points():
+    names = declared_functions()
+    for f in ("kvr_decode_attn", "kvr_accumulate_scores", "kvr_evict_topb", "kvr_logit_entropy"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2608_15797_amd import kvr
+    for name in declared_functions():
+        assert hasattr(kvr.lib, name), name
+    assert set(declared_functions()) == set(kvr.EXPORTS)
+
+
+def test_status_strings():
+    from paper_2608_15797_amd import kvr
+    assert kvr.lib.kvr_strerror(0) == b"ok"
+    assert kvr.lib.kvr_strerror(-1) == b"invalid argument"
+    assert kvr.lib.kvr_strerror(-4) == b"workspace missing or too small"
+
+
+def _cache(kvr, **kw):
+    d = dict(k=16, v=16, pos=None, S=2, L=1, Hkv=2, cap=33, D=128, dtype=1)
+    d.update(kw)
+    return kvr.c_cache(d["k"], d["v"], d["pos"], d["S"], d["L"], d["Hkv"], d["cap"], d["D"], d["dtype"])
+
+
+@pytest.mark.parametrize("kw,Hq,status,msg", [
+    (dict(k=None), 8, -1, "NULL"),
+    (dict(D=96), 8, -2, "head_dim"),
+    (dict(dtype=7), 8, -2, "dtype"),
+    (dict(S=0), 8, -1, "positive"),
+    ({}, 7, -1, "multiple"),
+    ({}, 34, -2, "exceeds 16"),
+    (dict(k=24), 8, -1, "aligned"),
+])
+def test_decode_attn_rejects_bad_arguments_on_host(kw, Hq, status, msg):
+    from paper_2608_15797_amd import kvr
+    c = _cache(kvr, **kw)
+    rc = kvr.lib.kvr_decode_attn(ctypes.byref(c), None, 16, 16, Hq, 1.0, None, None, None, 16,
+                                 None, None, None, 0, None)
+    assert rc == status
+    assert msg in kvr.lib.kvr_last_error().decode()
+
+
+def test_policy_validation_on_host():
+    from paper_2608_15797_amd import kvr
+    c = _cache(kvr, cap=20)
+    for pol, msg in ((kvr.c_policy(16, 8, 16), "cap="), (kvr.c_policy(16, 0, 4), "0 < W < B"),
+                     (kvr.c_policy(8, 4, 2), "buffer >= W-1")):
+        rc = kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, 16, ctypes.byref(pol), None, None)
+        assert rc == -1 and msg in kvr.lib.kvr_last_error().decode()
+
+
+def test_entropy_rejects_bad_arguments_on_host():
+    from paper_2608_15797_amd import kvr
+    assert kvr.lib.kvr_logit_entropy(16, 1, 4, 10, 5, 1.0, 16, None, None, 0, None) == -1
+    assert kvr.lib.kvr_logit_entropy(16, 3, 4, 10, 10, 1.0, 16, None, None, 0, None) == -2
+    # A split reduction needs a workspace.
+    need = kvr.lib.kvr_logit_entropy_workspace_size(8, 151936)
+    assert need > 0
+    assert kvr.lib.kvr_logit_entropy(16, 1, 8, 151936, 151936, 1.0, 16, None, None, 0, None) == -4
+
+
+def test_prefix_workspace_size_matches_split_plan():
+    from paper_2608_15797_amd import kvr
+    c = _cache(kvr, S=128, L=28, Hkv=2, cap=512)
+    p = kvr.c_prefix(16, 16, 16, 8192)
+    n = kvr.lib.kvr_decode_attn_workspace_size(ctypes.byref(c), ctypes.byref(p), 12)
+    rec = 128 * 28 * 12 * (128 + 4) * 4
+    assert n % rec == 0 and n // rec >= 2
