@@ -1,0 +1,284 @@
+"""Benchmark of the KV-Rescue candidate-decode hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the whole hot path over every candidate of the
+workload: base decode attention over the evicted cache with the streamed
+window score, top-B eviction when the cache overflows, helper decode attention
+over the full context, and full-vocabulary entropy with the detector. The
+default workload is the 7B-shaped base (16 problems x 8 candidates, B=64)
+interleaved with the 1.5B-shaped helper over 16 shared 8192-token contexts,
+with entropy over both models' logits; the 7B B=128 and 72B workloads are run
+after it and reported under "workloads".
+
+Inputs are synthetic and seeded, resident in HBM before timing starts. The
+prompt is decoded (teacher-forced) before timing; then W warmup steps, then
+exactly K timed steps between two synchronisations. A second, instrumented
+pass of K more steps brackets every library call with timing events to get
+per-call durations for the roofline. One JSON line is printed.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2608_15797_amd import accounting as acc  # noqa: E402
+from paper_2608_15797_amd.workloads import WORKLOADS  # noqa: E402
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "candidate decode steps/s (attn+evict+entropy)"
+DEFAULT_EXTRA = ("base7b", "base72b_helper")
+KERNEL_SOURCES = ("attn.hip", "evict.hip", "entropy.hip", "kvr_device.h")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_15797_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def step_bytes(wl, dec, i):
+    """Algorithmic bytes of decode step i by call name."""
+    out = {}
+    if wl.base:
+        b = wl.base
+        n = dec.blen_host[dec.T_prompt + i]
+        out["base_attn"] = acc.base_attn_bytes(wl, n)
+        if n > b.B + b.buffer:
+            out["evict"] = acc.evict_bytes(wl, n)
+    if wl.helper:
+        out["helper_attn"] = acc.helper_attn_bytes(wl, dec.hlen_host[i])
+    e = acc.esize(wl)
+    for w, ls in enumerate(wl.logits):
+        out["entropy%d" % w] = ls.R * ls.V * e + ls.R * 4
+    return out
+
+
+def run_workload(name, steps, warmup, instrument=True):
+    from paper_2608_15797_amd.pipeline import Decoder
+    base_wl = WORKLOADS[name]
+    steps = steps or base_wl.steps
+    wl = base_wl.with_(steps=warmup + (2 if instrument else 1) * steps)
+    t0 = time.time()
+    dec = Decoder(wl, device="cuda")
+    torch.cuda.synchronize()
+    log("[%s] buffers + input pool (%d draws) ready in %.1fs" % (name, len(dec.pool), time.time() - t0))
+    dec.prompt()
+    for i in range(warmup):
+        dec.step(i)
+    torch.cuda.synchronize()
+    log("[%s] prompt (%d tokens) + %d warmup steps done" % (name, dec.T_prompt, warmup))
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(warmup, warmup + steps):
+        dec.step(i)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end)
+    log("[%s] timed %d steps: %.3f ms/step" % (name, steps, ms / steps))
+
+    total = {}
+    for i in range(warmup, warmup + steps):
+        for k, v in step_bytes(wl, dec, i).items():
+            total[k] = total.get(k, 0) + v
+    all_bytes = sum(total.values())
+
+    calls = {}
+    if instrument:
+        timers = {}
+        for i in range(warmup + steps, warmup + 2 * steps):
+            dec.step(i, timers=timers)
+        torch.cuda.synchronize()
+        ibytes = {}
+        for i in range(warmup + steps, warmup + 2 * steps):
+            for k, v in step_bytes(wl, dec, i).items():
+                ibytes[k] = ibytes.get(k, 0) + v
+        for k, ev in timers.items():
+            dur = [s.elapsed_time(e) for s, e in ev]
+            n = len(dur)
+            avg_ms = sum(dur) / n
+            b_per = ibytes[k] / n
+            calls[k] = dict(launches=n, avg_us=round(avg_ms * 1e3, 2),
+                            bytes_per_call=int(b_per),
+                            GBps=round(b_per / (avg_ms * 1e-3) / 1e9, 1),
+                            frac=round(b_per / (avg_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4))
+        log("[%s] per-call: %s" % (name, json.dumps(calls)))
+
+    S = (wl.base.S if wl.base else 0) + (wl.helper.S if wl.helper else 0)
+    res = dict(workload=name, steps=steps, ms_per_step=ms / steps,
+               steps_per_s=steps / (ms * 1e-3), cand_tokens_per_s=S * steps / (ms * 1e-3),
+               alg_bytes_per_step=all_bytes / steps,
+               hbm_GBps=all_bytes / (ms * 1e-3) / 1e9,
+               hbm_frac=all_bytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, calls=calls)
+    return res, dec, wl
+
+
+def describe(wl):
+    d = {"workload": wl.name, "dtype": wl.dtype}
+    if wl.base:
+        b = wl.base
+        d["base"] = dict(S=b.S, L=b.L, Hq=b.Hq, Hkv=b.Hkv, D=b.D, B=b.B, W=b.W, buffer=b.buffer,
+                         prompt=b.prompt)
+    if wl.helper:
+        h = wl.helper
+        d["helper"] = dict(S=h.S, L=h.L, Hq=h.Hq, Hkv=h.Hkv, D=h.D, P=h.P, plen=h.plen, suffix=h.scap)
+    d["logits"] = [dict(R=ls.R, V=ls.V) for ls in wl.logits]
+    return d
+
+
+def traffic_for(name, kernel_key):
+    """HBM traffic of the dominant call measured by rocprofv3 PMC counters
+    (profiles/traffic_<workload>.json), if taken on the current kernels."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % name)
+    if not os.path.exists(path):
+        return None
+    t = json.load(open(path))
+    if t.get("kernel_source_hash") != kernel_source_hash() or t.get("call") != kernel_key:
+        return None
+    return t.get("bytes_per_call")
+
+
+def cpu_baseline(dec, wl, min_s=10.0):
+    """The fp64 oracle timed on this host, on a bounded sample of the same
+    workload: one problem's share of a decode step (its candidates' base
+    attention, helper attention and logit rows) at a time, problem after
+    problem and step after step, until at least `min_s` seconds of oracle
+    time; scaled to whole steps. Host copies are made outside the timing."""
+    import numpy as np
+
+    import oracle
+
+    def host(t):
+        t = t.detach().cpu().contiguous()
+        return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+
+    b, h = wl.base, wl.helper
+    problems = 8 if wl.name == "base72b_helper" else 16
+    secs, done = 0.0, 0
+    desc = []
+    for i in range(wl.steps):
+        t = dec.T_prompt + i
+        si = dec.inputs(t)
+        for p in range(problems):
+            if b:
+                nb = b.S // problems
+                sl = slice(p * nb, (p + 1) * nb)
+                n = dec.blen_host[t]
+                K, V, q = host(dec.bcache.k[sl]), host(dec.bcache.v[sl]), host(si.bq[sl])
+                t0 = time.perf_counter()
+                oracle.decode_attn(K, V, n, q, dec.bscale)
+                secs += time.perf_counter() - t0
+                if done == 0:
+                    desc.append("base %d of %d sequences" % (nb, b.S))
+            if h:
+                nh = h.S // problems
+                sl = slice(p * nh, (p + 1) * nh)
+                C = h.S // h.P
+                psl = slice((p * nh) // C, max((p * nh) // C + 1, ((p + 1) * nh) // C))
+                u = dec.hlen_host[i]
+                PK, PV = host(dec.prefix.k[psl]), host(dec.prefix.v[psl])
+                K, V, q = host(dec.hcache.k[sl]), host(dec.hcache.v[sl]), host(si.hq[sl])
+                t0 = time.perf_counter()
+                oracle.decode_attn(K, V, u, q, h.softmax_scale, prefix_K=PK, prefix_V=PV,
+                                   want_psum=False)
+                secs += time.perf_counter() - t0
+                if done == 0:
+                    desc.append("helper %d of %d candidates over context %d" % (nh, h.S, h.plen))
+            for w, ls in enumerate(wl.logits):
+                nr = max(1, ls.R // problems)
+                x = host(si.logits[w][p * nr:(p + 1) * nr])
+                t0 = time.perf_counter()
+                oracle.entropy(x, V=ls.V)
+                secs += time.perf_counter() - t0
+                if done == 0:
+                    desc.append("entropy %d of %d rows (V=%d)" % (nr, ls.R, ls.V))
+            done += 1
+            if secs >= min_s:
+                break
+        if secs >= min_s:
+            break
+    steps = done / problems
+    return dict(value=round(steps / secs, 6), unit="steps/s", cores=oracle.threads(), kind="oracle",
+                sample="%d problem-steps of %d problems per step (%s), %.1f s of oracle time"
+                % (done, problems, "; ".join(desc), secs))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=0, help="timed steps (default: the workload's decode steps)")
+    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--workload", default="base7b_helper", choices=sorted(WORKLOADS))
+    ap.add_argument("--extra", default=",".join(DEFAULT_EXTRA),
+                    help="comma-separated workloads also reported (empty: none)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-instrument", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    res, dec, wl = run_workload(args.workload, args.steps, args.warmup, not args.no_instrument)
+    steps = res["steps"]
+    calls = res["calls"]
+    roof = None
+    if calls:
+        dom = max(calls, key=lambda k: calls[k]["bytes_per_call"] * calls[k]["launches"])
+        c = calls[dom]
+        roof = dict(bound="hbm", achieved=c["GBps"], peak=PEAK_HBM_GBPS, unit="GB/s", frac=c["frac"],
+                    traffic=traffic_for(args.workload, dom), call=dom,
+                    alg_bytes_per_call=c["bytes_per_call"], avg_us=c["avg_us"])
+    cpu = None
+    if not args.no_cpu_baseline:
+        t0 = time.time()
+        cpu = cpu_baseline(dec, wl)
+        log("[cpu baseline] %.1fs: %s" % (time.time() - t0, json.dumps(cpu)))
+    del dec
+    torch.cuda.empty_cache()
+
+    extra = {}
+    for name in [x for x in args.extra.split(",") if x and x != args.workload]:
+        r, d, _ = run_workload(name, 0, args.warmup, not args.no_instrument)
+        del d
+        torch.cuda.empty_cache()
+        extra[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+
+    cfg = describe(WORKLOADS[args.workload])
+    cfg.update(cand_tokens_per_s=round(res["cand_tokens_per_s"], 1),
+               alg_bytes_per_step=int(res["alg_bytes_per_step"]),
+               hbm_GBps=round(res["hbm_GBps"], 1), hbm_frac_of_peak=round(res["hbm_frac"], 4),
+               calls=calls)
+    line = {
+        "metric": METRIC, "value": round(res["steps_per_s"], 3), "unit": "steps/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(res["ms_per_step"], 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, Qwen2.5-Math shapes)",
+        "config": cfg, "roofline": roof, "cpu_baseline": cpu, "workloads": extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -201,9 +201,9 @@ int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scor
  *            multiple of 16 (other ld values run a scalar path).
  *   H      : [R] float32 output.
  *   det    : NULL, or detector state updated with the new entropies.
- *   workspace : at least kvr_logit_entropy_workspace_size(R, V) bytes, zero
- *            filled before its first use; every completed call leaves it
- *            zeroed again. May be NULL/0 when that size is 0.
+ *   workspace : at least kvr_logit_entropy_workspace_size(R, V) bytes of
+ *            device scratch for per-split partial sums (no initialisation
+ *            needed). May be NULL/0 when that size is 0.
  * -inf logits are allowed (they contribute 0); a row of only -inf is invalid.
  */
 int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,

@@ -17,9 +17,12 @@
 //     four consecutive key rows (fully coalesced: 4 rows x 256 B per load
 //     instruction) and transposes 4x8 bf16 in registers with bit operations,
 //     which assigns output column n to d = n * (D/16) + b for instance b.
-// The softmax is online over chunks of 64 keys with running max and sum kept
-// in the log2 domain. Logits of window steps go to LDS so the normalised
-// probabilities can be summed over the G heads after the last chunk.
+// Keys stream in chunks of 32 through buffer loads (wave-uniform base and
+// range in SGPRs, 32-bit lane offsets, zero fill past the range), double
+// buffered so one chunk's loads are in flight while the previous one is
+// computed. The softmax is online with running max and sum kept in the log2
+// domain. Logits of window steps go to LDS so the normalised probabilities
+// can be summed over the G heads after the last chunk.
 //
 // Helper (prefix) path: split-K over the prefix; one wave per
 // (prefix, layer, KV head, split) processes the query rows of all candidates
@@ -70,29 +73,67 @@ __device__ __forceinline__ void load_qop(const bf16_t *qrow, int g4, short4_t (&
   }
 }
 
-// K operands of one key row with the same d mapping as load_qop.
-template <int D>
-__device__ __forceinline__ void load_krow(const bf16_t *krow, int g4, u32x4 (&w)[Geo<D>::NLD]) {
-#pragma unroll
-  for (int i = 0; i < Geo<D>::NLD; i++) {
-    if (krow)
-      w[i] = *reinterpret_cast<const u32x4 *>(krow + i * 32 + g4 * 8);
-    else
-      w[i] = u32x4{0u, 0u, 0u, 0u};
-  }
+// Buffer resources: a wave-uniform base address and byte range in SGPRs, so
+// per-lane addressing is a 32-bit offset and loads past the range return 0.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-// The lane's part of one V row: D/16 elements at n * (D/16).
-template <int D>
-__device__ __forceinline__ void load_vrow(const bf16_t *vrow, int r16, uint32_t (&w)[Geo<D>::VW]) {
-  if constexpr (D == 128) {
-    u32x4 x = {0u, 0u, 0u, 0u};
-    if (vrow) x = *reinterpret_cast<const u32x4 *>(vrow + r16 * 8);
-    w[0] = x.x; w[1] = x.y; w[2] = x.z; w[3] = x.w;
-  } else {
-    u32x2 x = {0u, 0u};
-    if (vrow) x = *reinterpret_cast<const u32x2 *>(vrow + r16 * 4);
-    w[0] = x.x; w[1] = x.y;
+// K and V data of one chunk of TILES*16 keys, as loaded by one lane:
+// k[t][i]: 16 bytes of key row c0 + 16t + (lane & 15) at d = 32i + 8*(lane >> 4);
+// v[t][c]: D/16 elements of value row c0 + 16t + 4*(lane >> 4) + c at d = (lane & 15) * D/16.
+template <int D, int TILES>
+struct KVChunk {
+  u32x4 k[TILES][Geo<D>::NLD];
+  uint32_t v[TILES][4][Geo<D>::VW];
+};
+
+template <int D, int TILES>
+__device__ __forceinline__ void load_chunk(KVChunk<D, TILES> &c, rsrc_t K, rsrc_t V, int c0,
+                                           int r16, int g4) {
+  constexpr uint32_t ROW = D * 2;
+#pragma unroll
+  for (int t = 0; t < TILES; t++) {
+    const uint32_t base = (uint32_t)(c0 + t * 16 + r16) * ROW + g4 * 16;
+#pragma unroll
+    for (int i = 0; i < Geo<D>::NLD; i++)
+      c.k[t][i] = __builtin_amdgcn_raw_buffer_load_b128(K, base + i * 64, 0, 0);
+  }
+#pragma unroll
+  for (int t = 0; t < TILES; t++)
+#pragma unroll
+    for (int cc = 0; cc < 4; cc++) {
+      const uint32_t off = (uint32_t)(c0 + t * 16 + 4 * g4 + cc) * ROW + r16 * (Geo<D>::NB * 2);
+      if constexpr (D == 128) {
+        const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(V, off, 0, 0);
+        c.v[t][cc][0] = x.x; c.v[t][cc][1] = x.y; c.v[t][cc][2] = x.z; c.v[t][cc][3] = x.w;
+      } else {
+        const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(V, off, 0, 0);
+        c.v[t][cc][0] = x.x; c.v[t][cc][1] = x.y;
+      }
+    }
+}
+
+// Logits (log2 domain) of one chunk for one 16-row block: S^T = K . Q^T.
+// Keys at or beyond nlim are masked to -inf.
+template <int D, int TILES>
+__device__ __forceinline__ void chunk_logits(const KVChunk<D, TILES> &c, const short4_t (&qop)[Geo<D>::NB],
+                                             float (&x)[TILES][4], int c0, int nlim, int g4, float sl2) {
+#pragma unroll
+  for (int t = 0; t < TILES; t++) {
+    float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < Geo<D>::NLD; i++) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(s4(c.k[t][i].x, c.k[t][i].y), qop[2 * i], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(s4(c.k[t][i].z, c.k[t][i].w), qop[2 * i + 1], acc, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int key = c0 + t * 16 + 4 * g4 + i;
+      x[t][i] = key < nlim ? acc[i] * sl2 : kNegInf;
+    }
   }
 }
 
@@ -160,10 +201,15 @@ __device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st,
 // ---------------------------------------------------------------------------
 // Own-cache kernel: base (evicted cache, optional score streaming) or helper
 // suffix (PARTIAL: writes a log-sum-exp partial into split slot nsplit).
+// Keys [0, n-1) stream from the cache in chunks of 32, double-buffered so the
+// next chunk's loads are in flight while the current one is computed; the
+// appended token (slot n-1) is a final one-key tile read from k_new/v_new.
 template <int D, bool PARTIAL>
 __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
-  constexpr int TILES = 4;
+  constexpr int TILES = 2;
+  constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
+  constexpr uint32_t ROW = D * 2;
   extern __shared__ float smem[];
 
   const int unit = blockIdx.x;  // ((s * L) + l) * Hkv + h
@@ -183,9 +229,10 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   bf16_t *Vc = static_cast<bf16_t *>(p.v) + ubase;
   const bf16_t *kn = p.k_new ? static_cast<const bf16_t *>(p.k_new) + (size_t)unit * D : nullptr;
   const bf16_t *vn = p.v_new ? static_cast<const bf16_t *>(p.v_new) + (size_t)unit * D : nullptr;
+  const bool append = kn != nullptr && n >= 1;
 
   // Append the new token at slot n-1 (reads below take it from k_new/v_new).
-  if (kn && n >= 1) {
+  if (append) {
     constexpr int LPR = D / 8;  // lanes per row, 16 bytes each
     if (lane < LPR) {
       reinterpret_cast<u32x4 *>(Kc + (size_t)(n - 1) * D)[lane] = reinterpret_cast<const u32x4 *>(kn)[lane];
@@ -196,6 +243,7 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
       p.pos[(size_t)unit * p.cap + n - 1] = p.new_pos[s];
     }
   }
+  const int ncache = append ? n - 1 : n;
 
   const int qh0 = h * G;
   const size_t qrow0 = ((size_t)s * p.L + l) * p.Hq + qh0;
@@ -215,42 +263,38 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
 #pragma unroll
   for (int b = 0; b < NB; b++) o[b] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int c0 = 0; c0 < n; c0 += 16 * TILES) {
-    u32x4 kr[TILES][Geo<D>::NLD];
-    uint32_t vr[TILES][4][Geo<D>::VW];
-#pragma unroll
-    for (int t = 0; t < TILES; t++) {
-      const int key = c0 + t * 16 + r16;
-      const bf16_t *krow = key < n ? ((kn && key == n - 1) ? kn : Kc + (size_t)key * D) : nullptr;
-      load_krow<D>(krow, g4, kr[t]);
-    }
-#pragma unroll
-    for (int t = 0; t < TILES; t++)
-#pragma unroll
-      for (int c = 0; c < 4; c++) {
-        const int key = c0 + t * 16 + 4 * g4 + c;
-        const bf16_t *vrow = key < n ? ((vn && key == n - 1) ? vn : Vc + (size_t)key * D) : nullptr;
-        load_vrow<D>(vrow, r16, vr[t][c]);
-      }
+  const rsrc_t Kr = make_rsrc(Kc, (uint32_t)ncache * ROW);
+  const rsrc_t Vr = make_rsrc(Vc, (uint32_t)ncache * ROW);
+  auto process = [&](const KVChunk<D, TILES> &c, int c0, int nlim) {
     float x[TILES][4];
+    chunk_logits<D, TILES>(c, qop, x, c0, nlim, g4, sl2);
+    if (win && r16 < G) {
 #pragma unroll
-    for (int t = 0; t < TILES; t++) {
-      float4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i = 0; i < Geo<D>::NLD; i++) {
-        acc = mfma16(s4(kr[t][i].x, kr[t][i].y), qop[2 * i], acc);
-        acc = mfma16(s4(kr[t][i].z, kr[t][i].w), qop[2 * i + 1], acc);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; i++) {
-        const int key = c0 + t * 16 + 4 * g4 + i;
-        x[t][i] = key < n ? acc[i] * sl2 : kNegInf;
-      }
-      if (win && r16 < G)
+      for (int t = 0; t < TILES; t++)
         *reinterpret_cast<float4_t *>(xs + r16 * ldx + c0 + t * 16 + 4 * g4) =
             float4_t{x[t][0], x[t][1], x[t][2], x[t][3]};
     }
-    softmax_pv<D, TILES>(x, st, o, vr, g4);
+    softmax_pv<D, TILES>(x, st, o, c.v, g4);
+  };
+
+  KVChunk<D, TILES> ca, cb;
+  if (ncache > 0) load_chunk<D, TILES>(ca, Kr, Vr, 0, r16, g4);
+  for (int c0 = 0; c0 < ncache; c0 += 2 * CH) {
+    const int c1 = c0 + CH;
+    if (c1 < ncache) load_chunk<D, TILES>(cb, Kr, Vr, c1, r16, g4);
+    process(ca, c0, ncache);
+    if (c1 >= ncache) break;
+    if (c1 + CH < ncache) load_chunk<D, TILES>(ca, Kr, Vr, c1 + CH, r16, g4);
+    process(cb, c1, ncache);
+  }
+  if (append) {
+    // One-key tile: only key row 0 of k_new/v_new is in range; the rest load 0.
+    KVChunk<D, 1> cn;
+    load_chunk<D, 1>(cn, make_rsrc(kn, ROW), make_rsrc(vn, ROW), 0, r16, g4);
+    float x[1][4];
+    chunk_logits<D, 1>(cn, qop, x, 0, 1, g4, sl2);
+    if (win && r16 < G && g4 == 0) xs[r16 * ldx + n - 1] = x[0][0];
+    softmax_pv<D, 1>(x, st, o, cn.v, g4);
   }
 
   float z = st.zl;
@@ -312,11 +356,15 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
 
 // ---------------------------------------------------------------------------
 // Prefix kernel: one wave per (prefix, layer, KV head, split); RB row blocks
-// of 16 rows hold the C*G query rows (candidate c, head g) sharing the prefix.
+// of 16 rows hold the C*G query rows (candidate c, head g) sharing the prefix,
+// so each prefix byte is read once per step for all of them. Same
+// double-buffered chunk stream as the own-cache kernel.
 template <int D, int RB>
 __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
-  constexpr int TILES = RB == 1 ? 4 : 2;
+  constexpr int TILES = 2;
+  constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
+  constexpr uint32_t ROW = D * 2;
   const int nunits = p.P * p.L * p.Hkv;
   const int split = blockIdx.x / nunits;
   const int unit = blockIdx.x % nunits;  // ((pp * L) + l) * Hkv + h
@@ -358,40 +406,26 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
     for (int b = 0; b < NB; b++) o[rb][b] = float4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int c0 = k0; c0 < k1; c0 += 16 * TILES) {
-    u32x4 kr[TILES][Geo<D>::NLD];
-    uint32_t vr[TILES][4][Geo<D>::VW];
-#pragma unroll
-    for (int t = 0; t < TILES; t++) {
-      const int key = c0 + t * 16 + r16;
-      load_krow<D>(key < k1 ? Kp + (size_t)key * D : nullptr, g4, kr[t]);
-    }
-#pragma unroll
-    for (int t = 0; t < TILES; t++)
-#pragma unroll
-      for (int c = 0; c < 4; c++) {
-        const int key = c0 + t * 16 + 4 * g4 + c;
-        load_vrow<D>(key < k1 ? Vp + (size_t)key * D : nullptr, r16, vr[t][c]);
-      }
+  // Byte range covers keys [0, k1); chunk offsets are absolute key indices.
+  const rsrc_t Kr = make_rsrc(Kp, (uint32_t)(k1 > 0 ? k1 : 0) * ROW);
+  const rsrc_t Vr = make_rsrc(Vp, (uint32_t)(k1 > 0 ? k1 : 0) * ROW);
+  auto process = [&](const KVChunk<D, TILES> &c, int c0) {
 #pragma unroll
     for (int rb = 0; rb < RB; rb++) {
       float x[TILES][4];
-#pragma unroll
-      for (int t = 0; t < TILES; t++) {
-        float4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int i = 0; i < Geo<D>::NLD; i++) {
-          acc = mfma16(s4(kr[t][i].x, kr[t][i].y), qop[rb][2 * i], acc);
-          acc = mfma16(s4(kr[t][i].z, kr[t][i].w), qop[rb][2 * i + 1], acc);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; i++) {
-          const int key = c0 + t * 16 + 4 * g4 + i;
-          x[t][i] = key < k1 ? acc[i] * sl2 : kNegInf;
-        }
-      }
-      softmax_pv<D, TILES>(x, st[rb], o[rb], vr, g4);
+      chunk_logits<D, TILES>(c, qop[rb], x, c0, k1, g4, sl2);
+      softmax_pv<D, TILES>(x, st[rb], o[rb], c.v, g4);
     }
+  };
+  KVChunk<D, TILES> ca, cb;
+  if (k0 < k1) load_chunk<D, TILES>(ca, Kr, Vr, k0, r16, g4);
+  for (int c0 = k0; c0 < k1; c0 += 2 * CH) {
+    const int c1 = c0 + CH;
+    if (c1 < k1) load_chunk<D, TILES>(cb, Kr, Vr, c1, r16, g4);
+    process(ca, c0);
+    if (c1 >= k1) break;
+    if (c1 + CH < k1) load_chunk<D, TILES>(ca, Kr, Vr, c1 + CH, r16, g4);
+    process(cb, c1);
   }
 
   float *ws = p.ws;

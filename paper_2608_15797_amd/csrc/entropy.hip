@@ -7,9 +7,16 @@
 // entropy is H = ln Z - (sum (x' - m') e^(x' - m')) / Z with x' the scaled
 // logits, in log2 units H = ln2 * (log2 Z - S / Z). Triples merge
 // associatively, first across a wave with shuffles, then across the
-// workgroup's waves, then across the workgroups that split a long row: every
-// split writes its triple to the workspace and the last one to finish (per-row
-// atomic counter, which it resets to zero) merges them and runs the detector.
+// workgroup's waves. When a row is split over several workgroups (so that a
+// few long rows still fill the chip), each writes its triple to the workspace
+// and a second, tiny kernel merges them per row and runs the detector. A
+// kernel boundary orders the two: merging inside the first kernel would need
+// device-scope fences, which on this chip write back and invalidate the
+// per-XCD L2 caches in every workgroup.
+//
+// Loads are buffer loads from a per-row resource (16 bytes per lane, zero
+// past the row), issued U at a time before any arithmetic, with values of
+// other splits masked by selects rather than branches.
 #include <hip/hip_runtime.h>
 
 #include "kvr_device.h"
@@ -67,21 +74,29 @@ __device__ __forceinline__ void tri_add(Tri &t, const float (&y)[N]) {
   }
 }
 
-__device__ __forceinline__ void load8(const bf16_t *ptr, float c, float (&y)[8]) {
-  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 w = *reinterpret_cast<const u32x4 *>(ptr);
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ rsrc_t row_rsrc(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// Vector v (8 logits) of a row through its buffer resource, scaled by c.
+__device__ __forceinline__ void load8(rsrc_t r, int v, float c, float (&y)[8], const bf16_t *) {
+  const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 16u, 0, 0);
   y[0] = bf16_lo(w.x) * c; y[1] = bf16_hi(w.x) * c;
   y[2] = bf16_lo(w.y) * c; y[3] = bf16_hi(w.y) * c;
   y[4] = bf16_lo(w.z) * c; y[5] = bf16_hi(w.z) * c;
   y[6] = bf16_lo(w.w) * c; y[7] = bf16_hi(w.w) * c;
 }
 
-__device__ __forceinline__ void load8(const float *ptr, float c, float (&y)[8]) {
-  typedef float f32x4 __attribute__((ext_vector_type(4)));
-  const f32x4 a = reinterpret_cast<const f32x4 *>(ptr)[0];
-  const f32x4 b = reinterpret_cast<const f32x4 *>(ptr)[1];
-  y[0] = a.x * c; y[1] = a.y * c; y[2] = a.z * c; y[3] = a.w * c;
-  y[4] = b.x * c; y[5] = b.y * c; y[6] = b.z * c; y[7] = b.w * c;
+__device__ __forceinline__ void load8(rsrc_t r, int v, float c, float (&y)[8], const float *) {
+  const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u, 0, 0);
+  const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u + 16u, 0, 0);
+  y[0] = __uint_as_float(a.x) * c; y[1] = __uint_as_float(a.y) * c;
+  y[2] = __uint_as_float(a.z) * c; y[3] = __uint_as_float(a.w) * c;
+  y[4] = __uint_as_float(b.x) * c; y[5] = __uint_as_float(b.y) * c;
+  y[6] = __uint_as_float(b.z) * c; y[7] = __uint_as_float(b.w) * c;
 }
 
 __device__ __forceinline__ float load1(const bf16_t *ptr) { return bf16_to_f32(*ptr); }
@@ -118,22 +133,45 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
 
   Tri t{kNegInf, 0.f, 0.f};
   if constexpr (VEC) {
+    // U vectors of 8 logits per thread per round, all loads issued first.
+    constexpr int U = 8;
     const int nvec = p.V / 8;
     const int per = (nvec + splits - 1) / splits;
     const int v0 = split * per;
     const int v1 = min(v0 + per, nvec);
-    int v = v0 + tid;
-    for (; v + kThreads < v1; v += 2 * kThreads) {
-      float a[8], b[8];
-      load8(x + (size_t)v * 8, c, a);
-      load8(x + (size_t)(v + kThreads) * 8, c, b);
-      tri_add<8>(t, a);
-      tri_add<8>(t, b);
-    }
-    if (v < v1) {
-      float a[8];
-      load8(x + (size_t)v * 8, c, a);
-      tri_add<8>(t, a);
+    const rsrc_t rr = row_rsrc(x, (uint32_t)p.V * (uint32_t)sizeof(T));
+    for (int base = v0 + tid; base < v1; base += U * kThreads) {
+      float y[U][8];
+#pragma unroll
+      for (int u = 0; u < U; u++) load8(rr, base + u * kThreads, c, y[u], x);
+#pragma unroll
+      for (int u = 0; u < U; u++) {
+        const bool ok = base + u * kThreads < v1;
+#pragma unroll
+        for (int e = 0; e < 8; e++) y[u][e] = ok ? y[u][e] : kNegInf;
+      }
+      float lm = kNegInf;
+#pragma unroll
+      for (int u = 0; u < U; u++)
+#pragma unroll
+        for (int e = 0; e < 8; e++) lm = fmaxf(lm, y[u][e]);
+      if (lm > t.m) {
+        if (t.z > 0.f) {
+          const float f = fast_exp2(t.m - lm);
+          t.s = (t.s + (t.m - lm) * t.z) * f;
+          t.z *= f;
+        }
+        t.m = lm;
+      }
+#pragma unroll
+      for (int u = 0; u < U; u++)
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+          const float d = fmaxf(y[u][e] - t.m, -256.0f);
+          const float w = fast_exp2(d);
+          t.z += w;
+          t.s = fmaf(d, w, t.s);
+        }
     }
     if (split == splits - 1) {
       const int e = nvec * 8 + tid;
@@ -170,27 +208,19 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
     detector_push(p, row, H);
     return;
   }
-  // Cross-workgroup merge: counters [R] (padded to 16 bytes), then partials
-  // [R][splits][4] floats.
-  int *cnt = static_cast<int *>(p.ws);
-  float *parts = reinterpret_cast<float *>(static_cast<char *>(p.ws) + (((size_t)p.R * 4 + 15) & ~(size_t)15));
-  float *mine = parts + ((size_t)row * splits + split) * 4;
+  float *mine = static_cast<float *>(p.ws) + ((size_t)row * splits + split) * 4;
   mine[0] = r.m;
   mine[1] = r.z;
   mine[2] = r.s;
-  __threadfence();
-  const int done = atomicAdd(&cnt[row], 1);
-  if (done != splits - 1) return;
-  __threadfence();
+}
+
+// Per-row merge of the split partials, then the detector; one thread per row.
+__global__ __launch_bounds__(256) void entropy_merge(EntropyParams p) {
+  const int row = blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= p.R) return;
+  const float *q = static_cast<const float *>(p.ws) + (size_t)row * p.splits * 4;
   Tri acc{kNegInf, 0.f, 0.f};
-  for (int k = 0; k < splits; k++) {
-    const float *q = parts + ((size_t)row * splits + k) * 4;
-    Tri o{__hip_atomic_load(q + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
-          __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
-          __hip_atomic_load(q + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)};
-    acc = tri_merge(acc, o);
-  }
-  cnt[row] = 0;
+  for (int k = 0; k < p.splits; k++) acc = tri_merge(acc, Tri{q[4 * k], q[4 * k + 1], q[4 * k + 2]});
   const float H = finish_entropy(acc);
   p.H[row] = H;
   detector_push(p, row, H);
@@ -213,7 +243,7 @@ int entropy_splits(int R, int V) {
 size_t entropy_workspace_bytes(int R, int V) {
   const int s = entropy_splits(R, V);
   if (s == 1) return 0;
-  return (((size_t)R * 4 + 15) & ~(size_t)15) + (size_t)R * s * 4 * sizeof(float);
+  return (size_t)R * s * 4 * sizeof(float);
 }
 
 hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream) {
@@ -227,6 +257,9 @@ hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream) {
     if (vec) hipLaunchKernelGGL((entropy_kernel<bf16_t, true>), grid, dim3(kThreads), 0, stream, p);
     else hipLaunchKernelGGL((entropy_kernel<bf16_t, false>), grid, dim3(kThreads), 0, stream, p);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.splits == 1) return e;
+  hipLaunchKernelGGL(entropy_merge, dim3((p.R + 255) / 256), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 

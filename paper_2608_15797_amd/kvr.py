@@ -122,13 +122,20 @@ class Cache:
         return Cache(k, v, pos)
 
     def c(self) -> c_cache:
+        cached = self.__dict__.get("_c")
+        if cached is not None and cached[0] == (self.k.data_ptr(), self.v.data_ptr(),
+                                                None if self.pos is None else self.pos.data_ptr()):
+            return cached[1]
         S, L, Hkv, cap, D = self.k.shape
         assert self.k.is_contiguous() and self.v.is_contiguous() and self.v.shape == self.k.shape
         if self.pos is not None:
             assert self.pos.shape == (S, L, Hkv, cap) and self.pos.dtype == torch.int32
-        return c_cache(self.k.data_ptr(), self.v.data_ptr(),
-                       None if self.pos is None else self.pos.data_ptr(),
-                       S, L, Hkv, cap, D, dtype_code(self.k.dtype))
+        cc = c_cache(self.k.data_ptr(), self.v.data_ptr(),
+                     None if self.pos is None else self.pos.data_ptr(),
+                     S, L, Hkv, cap, D, dtype_code(self.k.dtype))
+        self.__dict__["_c"] = ((self.k.data_ptr(), self.v.data_ptr(),
+                                None if self.pos is None else self.pos.data_ptr()), cc)
+        return cc
 
 
 @dataclass

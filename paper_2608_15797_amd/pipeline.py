@@ -153,44 +153,71 @@ class Decoder:
         return self.pool[t] if self.per_token else self.pool[t % len(self.pool)]
 
     # -- one token ------------------------------------------------------------
-    def base_token(self, t: int, si: StepInputs, stream=None, on_scored=None) -> bool:
+    def base_token(self, t: int, si: StepInputs, stream=None, on_scored=None,
+                   timers=None) -> bool:
         """Append + attend (+ score) for token t; evict if the cache overflows.
         Returns True when an eviction ran. `on_scored(t)` (tests) runs between
         the attention and the eviction."""
         b = self.wl.base
-        kvr.decode_attn(self.bcache, self.blen[t], si.bq, self.bout, self.bscale,
-                        k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,
-                        scores=self.scores, stream=stream)
+        with _timer(timers, "base_attn", stream):
+            kvr.decode_attn(self.bcache, self.blen[t], si.bq, self.bout, self.bscale,
+                            k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,
+                            scores=self.scores, stream=stream)
         if on_scored is not None:
             on_scored(t)
         if self.blen_host[t] > b.B + b.buffer:
-            kvr.evict_topb(self.bcache, self.blen[t], self.scores, self.policy, kept=self.kept,
-                           stream=stream)
+            with _timer(timers, "evict", stream):
+                kvr.evict_topb(self.bcache, self.blen[t], self.scores, self.policy,
+                               kept=self.kept, stream=stream)
             return True
         return False
 
-    def helper_token(self, step: int, si: StepInputs, stream=None) -> None:
+    def helper_token(self, step: int, si: StepInputs, stream=None, timers=None) -> None:
         h = self.wl.helper
-        kvr.decode_attn(self.hcache, self.hlen[step], si.hq, self.hout, h.softmax_scale,
-                        k_new=si.hk, v_new=si.hv, prefix=self.prefix, workspace=self.hws,
-                        stream=stream)
+        with _timer(timers, "helper_attn", stream):
+            kvr.decode_attn(self.hcache, self.hlen[step], si.hq, self.hout, h.softmax_scale,
+                            k_new=si.hk, v_new=si.hv, prefix=self.prefix, workspace=self.hws,
+                            stream=stream)
 
-    def entropy(self, si: StepInputs, stream=None) -> None:
+    def entropy(self, si: StepInputs, stream=None, timers=None) -> None:
         for w, lg in enumerate(si.logits):
-            kvr.logit_entropy(lg, self.H[w], V=self.wl.logits[w].V,
-                              detector=self.detector if w == 0 else None,
-                              workspace=self.ews[w], stream=stream)
+            with _timer(timers, "entropy%d" % w, stream):
+                kvr.logit_entropy(lg, self.H[w], V=self.wl.logits[w].V,
+                                  detector=self.detector if w == 0 else None,
+                                  workspace=self.ews[w], stream=stream)
 
     def prompt(self, stream=None) -> None:
         for t in range(self.T_prompt):
             self.base_token(t, self.inputs(t), stream)
 
-    def step(self, step: int, stream=None) -> None:
-        """Decode step `step` (0-based, after the prompt): the whole hot path."""
+    def step(self, step: int, stream=None, timers=None) -> None:
+        """Decode step `step` (0-based, after the prompt): the whole hot path.
+        With `timers` (a dict), each call is bracketed by a pair of timing
+        events on the launch stream, appended under its name."""
         t = self.T_prompt + step
         si = self.inputs(t)
         if self.wl.base:
-            self.base_token(t, si, stream)
+            self.base_token(t, si, stream, timers=timers)
         if self.wl.helper:
-            self.helper_token(step, si, stream)
-        self.entropy(si, stream)
+            self.helper_token(step, si, stream, timers=timers)
+        self.entropy(si, stream, timers=timers)
+
+
+class _timer:
+    """Context manager recording start/end events around one library call."""
+
+    def __init__(self, timers, key, stream):
+        self.timers, self.key, self.stream = timers, key, stream
+
+    def __enter__(self):
+        if self.timers is not None:
+            self.s = torch.cuda.Event(enable_timing=True)
+            self.s.record(self.stream)
+        return self
+
+    def __exit__(self, *exc):
+        if self.timers is not None:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(self.stream)
+            self.timers.setdefault(self.key, []).append((self.s, e))
+        return False
