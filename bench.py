@@ -131,6 +131,28 @@ def run_workload(name, steps, warmup, instrument=True):
     return res, dec, wl
 
 
+def copy_bandwidth(calibration=False, nbytes=1 << 30):
+    """Read+write bandwidth of a plain device-to-device copy of nbytes (a
+    measured reference beside the 8 TB/s nameplate). With calibration, the
+    copy runs three times so that profiler counters see a kernel of known
+    traffic (nbytes read, nbytes written per dispatch)."""
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    reps = 3 if calibration else 5
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e.record()
+    torch.cuda.synchronize()
+    gbps = 2 * nbytes * reps / (s.elapsed_time(e) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return round(gbps, 1)
+
+
 def describe(wl):
     d = {"workload": wl.name, "dtype": wl.dtype}
     if wl.base:
@@ -231,6 +253,9 @@ def main():
                     help="comma-separated workloads also reported (empty: none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-instrument", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 1 GiB device copy three times (reference for "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE scaling)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -239,6 +264,7 @@ def main():
         sys.exit(2)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    copy_ref = copy_bandwidth(calibration=args.copy_calibration)
 
     res, dec, wl = run_workload(args.workload, args.steps, args.warmup, not args.no_instrument)
     steps = res["steps"]
@@ -276,6 +302,7 @@ def main():
         "ms_per_step": round(res["ms_per_step"], 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, Qwen2.5-Math shapes)",
         "config": cfg, "roofline": roof, "cpu_baseline": cpu, "workloads": extra,
+        "copy_ref_GBps": copy_ref,
     }
     print(json.dumps(line), flush=True)
 

@@ -36,6 +36,7 @@
 #include "kvr_device.h"
 #include "kvr_internal.h"
 
+
 namespace kvr {
 
 namespace {
@@ -117,10 +118,12 @@ __device__ __forceinline__ void load_chunk(KVChunk<D, TILES> &c, rsrc_t K, rsrc_
 }
 
 // Logits (log2 domain) of one chunk for one 16-row block: S^T = K . Q^T.
-// Keys at or beyond nlim are masked to -inf.
+// Only a tail chunk (wave-uniform flag) can hold keys at or beyond nlim;
+// those are masked to -inf.
 template <int D, int TILES>
 __device__ __forceinline__ void chunk_logits(const KVChunk<D, TILES> &c, const short4_t (&qop)[Geo<D>::NB],
-                                             float (&x)[TILES][4], int c0, int nlim, int g4, float sl2) {
+                                             float (&x)[TILES][4], int c0, int nlim, int g4, float sl2,
+                                             bool tail) {
 #pragma unroll
   for (int t = 0; t < TILES; t++) {
     float4_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -130,24 +133,50 @@ __device__ __forceinline__ void chunk_logits(const KVChunk<D, TILES> &c, const s
       acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(s4(c.k[t][i].z, c.k[t][i].w), qop[2 * i + 1], acc, 0, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int key = c0 + t * 16 + 4 * g4 + i;
-      x[t][i] = key < nlim ? acc[i] * sl2 : kNegInf;
+    for (int i = 0; i < 4; i++) x[t][i] = acc[i] * sl2;
+    if (tail) {
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int key = c0 + t * 16 + 4 * g4 + i;
+        x[t][i] = key < nlim ? x[t][i] : kNegInf;
+      }
     }
   }
 }
 
-// B operand of P.V instance b from four V rows (keys 4*g4 + c, c = 0..3).
-template <int D>
-__device__ __forceinline__ short4_t vop(const uint32_t (&v)[4][Geo<D>::VW], int b) {
-  const int w = b >> 1;
-  if ((b & 1) == 0)
-    return s4((v[0][w] & 0xffffu) | (v[1][w] << 16), (v[2][w] & 0xffffu) | (v[3][w] << 16));
-  return s4((v[0][w] >> 16) | (v[1][w] & 0xffff0000u), (v[2][w] >> 16) | (v[3][w] & 0xffff0000u));
+// B operands of P.V for every instance b of every tile, from the four V rows
+// (keys 4*g4 + c, c = 0..3) each lane holds: operand b packs element b of
+// the four rows. Built once per chunk and shared by all row blocks.
+template <int D, int TILES>
+__device__ __forceinline__ void make_vops(const uint32_t (&v)[TILES][4][Geo<D>::VW],
+                                          short4_t (&vo)[TILES][Geo<D>::NB]) {
+#pragma unroll
+  for (int t = 0; t < TILES; t++)
+#pragma unroll
+    for (int w = 0; w < Geo<D>::VW; w++) {
+      vo[t][2 * w] = s4(__builtin_amdgcn_perm(v[t][1][w], v[t][0][w], 0x05040100u),
+                        __builtin_amdgcn_perm(v[t][3][w], v[t][2][w], 0x05040100u));
+      vo[t][2 * w + 1] = s4(__builtin_amdgcn_perm(v[t][1][w], v[t][0][w], 0x07060302u),
+                            __builtin_amdgcn_perm(v[t][3][w], v[t][2][w], 0x07060302u));
+    }
 }
 
+// Operand b of one tile, built on the fly (single-row-block kernels).
+template <int D>
+__device__ __forceinline__ short4_t make_vop(const uint32_t (&v)[4][Geo<D>::VW], int b) {
+  const int w = b >> 1;
+  const uint32_t sel = (b & 1) ? 0x07060302u : 0x05040100u;
+  return s4(__builtin_amdgcn_perm(v[1][w], v[0][w], sel), __builtin_amdgcn_perm(v[3][w], v[2][w], sel));
+}
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Four probabilities -> A operand of P.V (hardware round-to-nearest-even).
 __device__ __forceinline__ short4_t pop4(float a, float b, float c, float d) {
-  return s4(pack_bf16x2(a, b), pack_bf16x2(c, d));
+  const bf16x2_t lo = __builtin_convertvector((f32x2_t){a, b}, bf16x2_t);
+  const bf16x2_t hi = __builtin_convertvector((f32x2_t){c, d}, bf16x2_t);
+  return s4(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
 }
 
 // Online-softmax state of the lane's query row within one 16-row block.
@@ -159,10 +188,9 @@ struct RowState {
 // Process one chunk of TILES*16 keys for one row block. x[t][i] are the
 // lane's logits (log2 domain, masked = -inf). Updates state, rescales o and
 // accumulates P.V with the chunk's V rows.
-template <int D, int TILES>
-__device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st,
-                                           float4_t (&o)[Geo<D>::NB],
-                                           const uint32_t (&vr)[TILES][4][Geo<D>::VW], int g4) {
+template <int D, int TILES, bool LAZY, typename VOp>
+__device__ __forceinline__ void softmax_pv_core(float (&x)[TILES][4], RowState &st,
+                                                float4_t (&o)[Geo<D>::NB], VOp vop, int g4) {
   float cm = kNegInf;
 #pragma unroll
   for (int t = 0; t < TILES; t++)
@@ -182,20 +210,39 @@ __device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st,
       psum += x[t][i];
     }
   st.zl = st.zl * alpha + psum;
+  const bool grew = mn > st.m;
   st.m = mn;
-  // o rows are 4*g4 + i; their alphas live in lanes 4*g4 + i.
+  // o rows are 4*g4 + i; their alphas live in lanes 4*g4 + i. LAZY (long
+  // streams): once the running maxima settle no row grows and the rescale is
+  // skipped.
+  if (!LAZY || __any(grew)) {
 #pragma unroll
-  for (int i = 0; i < 4; i++) {
-    const float ai = __shfl(alpha, 4 * g4 + i, kWave);
+    for (int i = 0; i < 4; i++) {
+      const float ai = __shfl(alpha, 4 * g4 + i, kWave);
 #pragma unroll
-    for (int b = 0; b < Geo<D>::NB; b++) o[b][i] *= ai;
+      for (int b = 0; b < Geo<D>::NB; b++) o[b][i] *= ai;
+    }
   }
 #pragma unroll
   for (int t = 0; t < TILES; t++) {
     const short4_t pa = pop4(x[t][0], x[t][1], x[t][2], x[t][3]);
 #pragma unroll
-    for (int b = 0; b < Geo<D>::NB; b++) o[b] = mfma16(pa, vop<D>(vr[t], b), o[b]);
+    for (int b = 0; b < Geo<D>::NB; b++) o[b] = mfma16(pa, vop(t, b), o[b]);
   }
+}
+
+// With V operands prebuilt by make_vops (shared by several row blocks).
+template <int D, int TILES, bool LAZY = false>
+__device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st, float4_t (&o)[Geo<D>::NB],
+                                           const short4_t (&vo)[TILES][Geo<D>::NB], int g4) {
+  softmax_pv_core<D, TILES, LAZY>(x, st, o, [&](int t, int b) { return vo[t][b]; }, g4);
+}
+
+// With V operands built on the fly from the raw rows.
+template <int D, int TILES, bool LAZY = false>
+__device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st, float4_t (&o)[Geo<D>::NB],
+                                           const uint32_t (&v)[TILES][4][Geo<D>::VW], int g4) {
+  softmax_pv_core<D, TILES, LAZY>(x, st, o, [&](int t, int b) { return make_vop<D>(v[t], b); }, g4);
 }
 
 // ---------------------------------------------------------------------------
@@ -267,7 +314,7 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   const rsrc_t Vr = make_rsrc(Vc, (uint32_t)ncache * ROW);
   auto process = [&](const KVChunk<D, TILES> &c, int c0, int nlim) {
     float x[TILES][4];
-    chunk_logits<D, TILES>(c, qop, x, c0, nlim, g4, sl2);
+    chunk_logits<D, TILES>(c, qop, x, c0, nlim, g4, sl2, c0 + CH > nlim);
     if (win && r16 < G) {
 #pragma unroll
       for (int t = 0; t < TILES; t++)
@@ -277,8 +324,31 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
     softmax_pv<D, TILES>(x, st, o, c.v, g4);
   };
 
+  // Every load a unit needs is issued up front so that only one memory round
+  // trip is exposed per unit: the new token's one-key tile (processed first;
+  // key order does not matter to the online softmax), the first cache chunk,
+  // and, in window steps that accumulate, the stored scores.
+  KVChunk<D, 1> cn;
+  if (append) load_chunk<D, 1>(cn, make_rsrc(kn, ROW), make_rsrc(vn, ROW), 0, r16, g4);
   KVChunk<D, TILES> ca, cb;
   if (ncache > 0) load_chunk<D, TILES>(ca, Kr, Vr, 0, r16, g4);
+  constexpr int PRE = 5;  // stored scores prefetched per lane (slots < 320)
+  const bool accumulate = win && n != wstart;
+  float old[PRE];
+  float *sc = win ? p.scores + (size_t)unit * p.cap : nullptr;
+  if (accumulate) {
+    const rsrc_t Sr = make_rsrc(sc, (uint32_t)(n - 1) * 4u);
+#pragma unroll
+    for (int k = 0; k < PRE; k++)
+      old[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(Sr, (uint32_t)(lane + 64 * k) * 4u, 0, 0));
+  }
+  float xnew = kNegInf;  // the new token's logit, stored after the tail chunk's masked ones
+  if (append) {
+    float x[1][4];
+    chunk_logits<D, 1>(cn, qop, x, 0, 1, g4, sl2, true);
+    xnew = x[0][0];
+    softmax_pv<D, 1>(x, st, o, cn.v, g4);
+  }
   for (int c0 = 0; c0 < ncache; c0 += 2 * CH) {
     const int c1 = c0 + CH;
     if (c1 < ncache) load_chunk<D, TILES>(cb, Kr, Vr, c1, r16, g4);
@@ -287,15 +357,7 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
     if (c1 + CH < ncache) load_chunk<D, TILES>(ca, Kr, Vr, c1 + CH, r16, g4);
     process(cb, c1, ncache);
   }
-  if (append) {
-    // One-key tile: only key row 0 of k_new/v_new is in range; the rest load 0.
-    KVChunk<D, 1> cn;
-    load_chunk<D, 1>(cn, make_rsrc(kn, ROW), make_rsrc(vn, ROW), 0, r16, g4);
-    float x[1][4];
-    chunk_logits<D, 1>(cn, qop, x, 0, 1, g4, sl2);
-    if (win && r16 < G && g4 == 0) xs[r16 * ldx + n - 1] = x[0][0];
-    softmax_pv<D, 1>(x, st, o, cn.v, g4);
-  }
+  if (append && win && r16 < G && g4 == 0) xs[r16 * ldx + n - 1] = xnew;
 
   float z = st.zl;
   z += shfl_xor(z, 16);
@@ -340,15 +402,21 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
         stat[16 + r16] = 1.0f / z;
       }
       __syncthreads();
-      const bool first = n == wstart;
-      float *sc = p.scores + (size_t)unit * p.cap;
-      for (int j = lane; j < n; j += kWave) {
+      // Slot n-1 (the new token) and the first window step store; older slots
+      // add to the stored score (prefetched above for the first PRE*64 slots).
+#pragma unroll
+      for (int k = 0; k < PRE; k++) {
+        const int j = lane + 64 * k;
+        if (j < n) {
+          float r = 0.0f;
+          for (int g = 0; g < G; g++) r += fast_exp2(xs[g * ldx + j] - stat[g]) * stat[16 + g];
+          sc[j] = (accumulate && j < n - 1) ? old[k] + r : r;
+        }
+      }
+      for (int j = lane + 64 * PRE; j < n; j += kWave) {
         float r = 0.0f;
         for (int g = 0; g < G; g++) r += fast_exp2(xs[g * ldx + j] - stat[g]) * stat[16 + g];
-        if (first || j == n - 1)
-          sc[j] = r;
-        else
-          sc[j] += r;
+        sc[j] = (accumulate && j < n - 1) ? sc[j] + r : r;
       }
     }
   }
@@ -410,11 +478,23 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
   const rsrc_t Kr = make_rsrc(Kp, (uint32_t)(k1 > 0 ? k1 : 0) * ROW);
   const rsrc_t Vr = make_rsrc(Vp, (uint32_t)(k1 > 0 ? k1 : 0) * ROW);
   auto process = [&](const KVChunk<D, TILES> &c, int c0) {
+    const bool tail = c0 + CH > k1;
+    if constexpr (RB == 2 || RB == 3) {
+      short4_t vo[TILES][NB];
+      make_vops<D, TILES>(c.v, vo);
 #pragma unroll
-    for (int rb = 0; rb < RB; rb++) {
-      float x[TILES][4];
-      chunk_logits<D, TILES>(c, qop[rb], x, c0, k1, g4, sl2);
-      softmax_pv<D, TILES>(x, st[rb], o[rb], c.v, g4);
+      for (int rb = 0; rb < RB; rb++) {
+        float x[TILES][4];
+        chunk_logits<D, TILES>(c, qop[rb], x, c0, k1, g4, sl2, tail);
+        softmax_pv<D, TILES, true>(x, st[rb], o[rb], vo, g4);
+      }
+    } else {
+#pragma unroll
+      for (int rb = 0; rb < RB; rb++) {
+        float x[TILES][4];
+        chunk_logits<D, TILES>(c, qop[rb], x, c0, k1, g4, sl2, tail);
+        softmax_pv<D, TILES, false>(x, st[rb], o[rb], c.v, g4);
+      }
     }
   };
   KVChunk<D, TILES> ca, cb;

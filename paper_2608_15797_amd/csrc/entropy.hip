@@ -14,9 +14,10 @@
 // device-scope fences, which on this chip write back and invalidate the
 // per-XCD L2 caches in every workgroup.
 //
-// Loads are buffer loads from a per-row resource (16 bytes per lane, zero
-// past the row), issued U at a time before any arithmetic, with values of
-// other splits masked by selects rather than branches.
+// Loads are buffer loads from a per-split resource (16 bytes per lane; lanes
+// past the split's range return zero without touching memory), issued U at a
+// time before any arithmetic, with invalid values masked by selects rather
+// than branches.
 #include <hip/hip_runtime.h>
 
 #include "kvr_device.h"
@@ -139,7 +140,9 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
     const int per = (nvec + splits - 1) / splits;
     const int v0 = split * per;
     const int v1 = min(v0 + per, nvec);
-    const rsrc_t rr = row_rsrc(x, (uint32_t)p.V * (uint32_t)sizeof(T));
+    // The resource ends where this split's vectors end, so the lanes of a
+    // partly used round load nothing instead of fetching the next split.
+    const rsrc_t rr = row_rsrc(x, (uint32_t)v1 * 8u * (uint32_t)sizeof(T));
     for (int base = v0 + tid; base < v1; base += U * kThreads) {
       float y[U][8];
 #pragma unroll

@@ -277,6 +277,39 @@ def test_evict_topb_planted(case):
     assert np.array_equal(pg, ph)
 
 
+@pytest.mark.parametrize("S,L,Hkv,B,W,buffer", [(64, 28, 4, 128, 32, 128), (32, 80, 8, 64, 32, 64)])
+def test_evict_topb_planted_full_shape(S, L, Hkv, B, W, buffer):
+    """Full workload shapes (7B: 64 x 28 x 4 heads, cap 257; 72B: 32 x 80 x 8,
+    cap 129) with planted scores separated by >= 1.5e-3: every kept set equals
+    the oracle's bit for bit, and the compaction moves exactly those rows."""
+    k = kvr()
+    D, cap = 128, B + buffer + 1
+    g = torch.Generator().manual_seed(S * L + B)
+    n = cap - W
+    base = torch.arange(n, dtype=torch.float64) * 2e-3
+    perm = torch.argsort(torch.rand((S, L, Hkv, n), generator=g), dim=-1)
+    sc = torch.zeros((S, L, Hkv, cap), dtype=torch.float32)
+    sc[..., :n] = (0.5 + base[perm] + torch.rand((S, L, Hkv, n), generator=g, dtype=torch.float64) * 5e-4).float()
+    # Row j of every head holds the value j in all of its elements, so the
+    # compacted cache reveals which rows moved where.
+    rowid = torch.arange(cap, dtype=torch.float32).view(1, 1, 1, cap, 1)
+    K = (rowid * 0.5).expand(S, L, Hkv, cap, D).to(torch.bfloat16).contiguous()
+    V = (rowid * 0.25).expand(S, L, Hkv, cap, D).to(torch.bfloat16).contiguous()
+    cache = k.Cache(K.to(DEV), V.to(DEV), torch.arange(cap, dtype=torch.int32).repeat(S, L, Hkv, 1).to(DEV))
+    kept = torch.empty((S, L, Hkv, B), dtype=torch.int32, device=DEV)
+    k.evict_topb(cache, torch.full((S,), cap, dtype=torch.int32, device=DEV), sc.to(DEV),
+                 k.Policy(B, W, buffer), kept=kept)
+    torch.cuda.synchronize()
+    kg = kept.cpu().numpy()
+    scn = sc.double().numpy()
+    for idx in np.ndindex(S, L, Hkv):
+        ref = oracle.select_topb(scn[idx], cap, B, W)
+        assert np.array_equal(kg[idx], ref), idx
+    assert np.array_equal(cache.pos.cpu().numpy()[..., :B], kg)
+    Kg = cache.k[..., :B, :].float().cpu()
+    assert torch.equal(Kg, (torch.from_numpy(kg).float() * 0.5)[..., None].expand_as(Kg).to(torch.bfloat16).float())
+
+
 def test_evict_topb_ties_and_gpu_scores_selection():
     """Exact ties go to the lower slot (integer-valued scores)."""
     k = kvr()
