@@ -27,8 +27,9 @@
 // Helper (prefix) path: split-K over the prefix; one wave per
 // (prefix, layer, KV head, split) processes the query rows of all candidates
 // sharing the prefix (up to 4 row blocks = 64 rows), so shared context is
-// read from HBM once per step. The private suffix runs as its own unit. Both
-// write (max, sum, unnormalised o) partials, merged by log-sum-exp.
+// read from HBM once per step, and writes (max, sum, unnormalised o)
+// partials. The private suffix then runs as its own unit per (candidate,
+// layer, KV head) and folds those partials in by log-sum-exp.
 //
 // f32 path: plain VALU kernel (one wave per unit) for float32 caches.
 #include <hip/hip_runtime.h>
@@ -144,6 +145,30 @@ __device__ __forceinline__ void chunk_logits(const KVChunk<D, TILES> &c, const s
   }
 }
 
+// Stream chunks of CH = 16*TILES keys over [k0, k1) through a DEPTH-deep ring
+// of register buffers: DEPTH-1 chunks are in flight while one is processed.
+// Loads past the resource's range return zero without touching memory, so
+// the ring is refilled unconditionally; pre() runs once the first loads are
+// in flight, then proc(chunk, c0) sees each real chunk.
+template <int D, int TILES, int DEPTH, typename Pre, typename Proc>
+__device__ __forceinline__ void stream_chunks(rsrc_t K, rsrc_t V, int k0, int k1, int r16, int g4,
+                                              Pre pre, Proc proc) {
+  constexpr int stride = 16 * TILES;
+  KVChunk<D, TILES> buf[DEPTH];
+#pragma unroll
+  for (int s = 0; s < DEPTH - 1; s++) load_chunk<D, TILES>(buf[s], K, V, k0 + s * stride, r16, g4);
+  pre();
+  for (int c0 = k0; c0 < k1; c0 += DEPTH * stride) {
+#pragma unroll
+    for (int j = 0; j < DEPTH; j++) {
+      const int cj = c0 + j * stride;
+      if (cj >= k1) break;
+      load_chunk<D, TILES>(buf[(j + DEPTH - 1) % DEPTH], K, V, cj + (DEPTH - 1) * stride, r16, g4);
+      proc(buf[j], cj);
+    }
+  }
+}
+
 // B operands of P.V for every instance b of every tile, from the four V rows
 // (keys 4*g4 + c, c = 0..3) each lane holds: operand b packs element b of
 // the four rows. Built once per chunk and shared by all row blocks.
@@ -247,13 +272,14 @@ __device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st, f
 
 // ---------------------------------------------------------------------------
 // Own-cache kernel: base (evicted cache, optional score streaming) or helper
-// suffix (PARTIAL: writes a log-sum-exp partial into split slot nsplit).
+// suffix (MERGE: runs after the context kernel on the same stream and folds
+// that kernel's split partials of its rows into its own softmax state before
+// writing the output, so no separate merge pass is needed).
 // Keys [0, n-1) stream from the cache in chunks of 32, double-buffered so the
 // next chunk's loads are in flight while the current one is computed; the
 // appended token (slot n-1) is a final one-key tile read from k_new/v_new.
-template <int D, bool PARTIAL>
+template <int D, bool MERGE, int TILES, int DEPTH>
 __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
-  constexpr int TILES = 2;
   constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
   constexpr uint32_t ROW = D * 2;
@@ -299,7 +325,7 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
 
   // Observation-window step of this sequence?
   const int wstart = p.B + p.buffer + 2 - p.W;
-  const bool win = !PARTIAL && p.scores != nullptr && n >= wstart;
+  const bool win = !MERGE && p.scores != nullptr && n >= wstart;
   const int ldx = (p.cap + 63) & ~63;
   float *xs = smem;                 // [G][ldx] logits of window steps
   float *stat = smem + G * ldx;     // [16] max, [16] 1/sum
@@ -330,8 +356,6 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   // and, in window steps that accumulate, the stored scores.
   KVChunk<D, 1> cn;
   if (append) load_chunk<D, 1>(cn, make_rsrc(kn, ROW), make_rsrc(vn, ROW), 0, r16, g4);
-  KVChunk<D, TILES> ca, cb;
-  if (ncache > 0) load_chunk<D, TILES>(ca, Kr, Vr, 0, r16, g4);
   constexpr int PRE = 5;  // stored scores prefetched per lane (slots < 320)
   const bool accumulate = win && n != wstart;
   float old[PRE];
@@ -343,59 +367,63 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
       old[k] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(Sr, (uint32_t)(lane + 64 * k) * 4u, 0, 0));
   }
   float xnew = kNegInf;  // the new token's logit, stored after the tail chunk's masked ones
-  if (append) {
-    float x[1][4];
-    chunk_logits<D, 1>(cn, qop, x, 0, 1, g4, sl2, true);
-    xnew = x[0][0];
-    softmax_pv<D, 1>(x, st, o, cn.v, g4);
-  }
-  for (int c0 = 0; c0 < ncache; c0 += 2 * CH) {
-    const int c1 = c0 + CH;
-    if (c1 < ncache) load_chunk<D, TILES>(cb, Kr, Vr, c1, r16, g4);
-    process(ca, c0, ncache);
-    if (c1 >= ncache) break;
-    if (c1 + CH < ncache) load_chunk<D, TILES>(ca, Kr, Vr, c1 + CH, r16, g4);
-    process(cb, c1, ncache);
-  }
+  auto new_token = [&]() {
+    if (append) {
+      float x[1][4];
+      chunk_logits<D, 1>(cn, qop, x, 0, 1, g4, sl2, true);
+      xnew = x[0][0];
+      softmax_pv<D, 1>(x, st, o, cn.v, g4);
+    }
+  };
+  stream_chunks<D, TILES, DEPTH>(Kr, Vr, 0, ncache, r16, g4, new_token,
+                                 [&](const KVChunk<D, TILES> &c, int c0) { process(c, c0, ncache); });
   if (append && win && r16 < G && g4 == 0) xs[r16 * ldx + n - 1] = xnew;
 
   float z = st.zl;
   z += shfl_xor(z, 16);
   z += shfl_xor(z, 32);
 
-  if constexpr (PARTIAL) {
-    float *ws = p.ws;
+  bf16_t *out = static_cast<bf16_t *>(p.out);
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int row = 4 * g4 + i;
+  for (int i = 0; i < 4; i++) {
+    const int row = 4 * g4 + i;
+    float zi = __shfl(z, row, kWave);
+    if constexpr (MERGE) {
+      // Log-sum-exp merge with the context partials of this row:
+      // record = (max, sum, -, -, unnormalised o[D]) in the log2 domain.
       const float mi = __shfl(st.m, row, kWave);
-      const float zi = __shfl(z, row, kWave);
       if (row < G) {
-        const size_t rec = (((size_t)p.nsplit * p.S + s) * p.L + l) * p.Hq + qh0 + row;
-        float *r = ws + rec * (D + 4);
-        if (r16 == 0) { r[0] = mi; r[1] = zi; }
+        const size_t stride = (size_t)p.S * p.L * p.Hq * (D + 4);
+        const float *r0 = p.ws + ((((size_t)s * p.L + l) * p.Hq + qh0 + row) * (D + 4));
+        float M = mi;
+        for (int k = 0; k < p.nsplit; k++) M = fmaxf(M, r0[k * stride]);
+        const float wown = fast_exp2(mi - M);
+        zi *= wown;
 #pragma unroll
-        for (int b = 0; b < NB; b++) r[4 + r16 * NB + b] = o[b][i];
+        for (int b = 0; b < NB; b++) o[b][i] *= wown;
+        for (int k = 0; k < p.nsplit; k++) {
+          const float *r = r0 + k * stride;
+          const float mk = r[0];
+          const float w = mk == kNegInf ? 0.0f : fast_exp2(mk - M);
+          zi += r[1] * w;
+#pragma unroll
+          for (int b = 0; b < NB; b++) o[b][i] += r[4 + r16 * NB + b] * w;
+        }
       }
     }
-  } else {
-    bf16_t *out = static_cast<bf16_t *>(p.out);
+    if (row < G) {
+      const float inv = 1.0f / zi;
+      uint32_t w[NB / 2];
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int row = 4 * g4 + i;
-      const float zi = __shfl(z, row, kWave);
-      if (row < G) {
-        const float inv = 1.0f / zi;
-        uint32_t w[NB / 2];
-#pragma unroll
-        for (int b = 0; b < NB / 2; b++) w[b] = pack_bf16x2(o[2 * b][i] * inv, o[2 * b + 1][i] * inv);
-        bf16_t *dst = out + (qrow0 + row) * D + r16 * NB;
-        if constexpr (D == 128)
-          *reinterpret_cast<u32x4 *>(dst) = u32x4{w[0], w[1], w[2], w[3]};
-        else
-          *reinterpret_cast<u32x2 *>(dst) = u32x2{w[0], w[1]};
-      }
+      for (int b = 0; b < NB / 2; b++) w[b] = pack_bf16x2(o[2 * b][i] * inv, o[2 * b + 1][i] * inv);
+      bf16_t *dst = out + (qrow0 + row) * D + r16 * NB;
+      if constexpr (D == 128)
+        *reinterpret_cast<u32x4 *>(dst) = u32x4{w[0], w[1], w[2], w[3]};
+      else
+        *reinterpret_cast<u32x2 *>(dst) = u32x2{w[0], w[1]};
     }
+  }
+  if constexpr (!MERGE) {
     if (win) {
       if (g4 == 0 && r16 < G) {
         stat[r16] = st.m;
@@ -427,9 +455,8 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
 // of 16 rows hold the C*G query rows (candidate c, head g) sharing the prefix,
 // so each prefix byte is read once per step for all of them. Same
 // double-buffered chunk stream as the own-cache kernel.
-template <int D, int RB>
+template <int D, int RB, int TILES, int DEPTH>
 __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
-  constexpr int TILES = 2;
   constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
   constexpr uint32_t ROW = D * 2;
@@ -497,16 +524,7 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
       }
     }
   };
-  KVChunk<D, TILES> ca, cb;
-  if (k0 < k1) load_chunk<D, TILES>(ca, Kr, Vr, k0, r16, g4);
-  for (int c0 = k0; c0 < k1; c0 += 2 * CH) {
-    const int c1 = c0 + CH;
-    if (c1 < k1) load_chunk<D, TILES>(cb, Kr, Vr, c1, r16, g4);
-    process(ca, c0);
-    if (c1 >= k1) break;
-    if (c1 + CH < k1) load_chunk<D, TILES>(ca, Kr, Vr, c1 + CH, r16, g4);
-    process(cb, c1);
-  }
+  stream_chunks<D, TILES, DEPTH>(Kr, Vr, k0, k1, r16, g4, [] {}, process);
 
   float *ws = p.ws;
 #pragma unroll
@@ -531,40 +549,6 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
       }
     }
   }
-}
-
-// Log-sum-exp merge of nsplit + 1 partials per query row; one wave per row.
-template <int D>
-__global__ __launch_bounds__(256) void attn_merge_bf16(AttnParams p) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  const int nrows = p.S * p.L * p.Hq;
-  if (row >= nrows) return;
-  const int nparts = p.nsplit + 1;
-  const size_t stride = (size_t)nrows * (D + 4);
-  const float *base = p.ws + (size_t)row * (D + 4);
-  float M = kNegInf;
-  for (int k = 0; k < nparts; k++) M = fmaxf(M, base[k * stride]);
-  constexpr int PER = D / 64;
-  float acc[PER];
-#pragma unroll
-  for (int e = 0; e < PER; e++) acc[e] = 0.f;
-  float Z = 0.f;
-  for (int k = 0; k < nparts; k++) {
-    const float *r = base + k * stride;
-    const float w = r[0] == kNegInf ? 0.f : fast_exp2(r[0] - M);
-    Z += r[1] * w;
-    // record layout: o element for lane-of-origin n, instance b at 4 + n*NB + b,
-    // i.e. d = n*NB + b maps to record index 4 + d.
-#pragma unroll
-    for (int e = 0; e < PER; e++) acc[e] += r[4 + lane * PER + e] * w;
-  }
-  const float inv = 1.0f / Z;
-  bf16_t *out = static_cast<bf16_t *>(p.out) + (size_t)row * D + lane * PER;
-  if constexpr (PER == 2)
-    *reinterpret_cast<uint32_t *>(out) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
-  else
-    out[0] = (bf16_t)f32_to_bf16_bits(acc[0] * inv);
 }
 
 // ---------------------------------------------------------------------------
@@ -661,27 +645,25 @@ __global__ __launch_bounds__(64) void attn_f32(AttnParams p, int nt_max) {
 
 template <int D>
 hipError_t launch_bf16(const AttnParams &p, hipStream_t stream) {
+  const dim3 units(p.S * p.L * p.Hkv);
   if (p.P == 0) {
     const size_t lds = p.scores ? ((size_t)p.G * ((p.cap + 63) & ~63) + 32) * sizeof(float) : 0;
-    hipLaunchKernelGGL((attn_cache_bf16<D, false>), dim3(p.S * p.L * p.Hkv), dim3(64), lds, stream, p);
+    hipLaunchKernelGGL((attn_cache_bf16<D, false, 2, 2>), units, dim3(64), lds, stream, p);
     return hipGetLastError();
   }
+  // Context splits first; the suffix kernel then merges their partials.
   const int rb = (p.C * p.G + 15) / 16;
   const dim3 gridA(p.P * p.L * p.Hkv * p.nsplit);
   switch (rb) {
-    case 1: hipLaunchKernelGGL((attn_prefix_bf16<D, 1>), gridA, dim3(64), 0, stream, p); break;
-    case 2: hipLaunchKernelGGL((attn_prefix_bf16<D, 2>), gridA, dim3(64), 0, stream, p); break;
-    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3>), gridA, dim3(64), 0, stream, p); break;
-    case 4: hipLaunchKernelGGL((attn_prefix_bf16<D, 4>), gridA, dim3(64), 0, stream, p); break;
+    case 1: hipLaunchKernelGGL((attn_prefix_bf16<D, 1, 2, 2>), gridA, dim3(64), 0, stream, p); break;
+    case 2: hipLaunchKernelGGL((attn_prefix_bf16<D, 2, 2, 2>), gridA, dim3(64), 0, stream, p); break;
+    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3, 2, 2>), gridA, dim3(64), 0, stream, p); break;
+    case 4: hipLaunchKernelGGL((attn_prefix_bf16<D, 4, 1, 2>), gridA, dim3(64), 0, stream, p); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_cache_bf16<D, true>), dim3(p.S * p.L * p.Hkv), dim3(64), 0, stream, p);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int nrows = p.S * p.L * p.Hq;
-  hipLaunchKernelGGL((attn_merge_bf16<D>), dim3((nrows + 3) / 4), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL((attn_cache_bf16<D, true, 2, 2>), units, dim3(64), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -707,7 +689,7 @@ void plan_prefix_splits(int P, int L, int Hkv, int plen, int *nsplit, int *chunk
 }
 
 size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit) {
-  return (size_t)(nsplit + 1) * S * L * Hq * (D + 4) * sizeof(float);
+  return (size_t)nsplit * S * L * Hq * (D + 4) * sizeof(float);
 }
 
 hipError_t launch_decode_attn(const AttnParams &p, hipStream_t stream) {

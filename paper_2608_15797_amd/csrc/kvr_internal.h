@@ -26,7 +26,7 @@ struct AttnParams {
   // scoring (scores == nullptr: off)
   float *scores;
   int B, W, buffer;
-  // split-K partials for the prefix path: ws [nsplit+1][S][L][Hq][D+4] floats
+  // split-K partials for the prefix path: ws [nsplit][S][L][Hq][D+4] floats
   float *ws;
   int nsplit, chunk;
 };
