@@ -20,7 +20,6 @@ per-call durations for the roofline. One JSON line is printed.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -32,22 +31,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 from paper_2608_15797_amd import accounting as acc  # noqa: E402
+from paper_2608_15797_amd.profsum import kernel_source_hash  # noqa: E402
 from paper_2608_15797_amd.workloads import WORKLOADS  # noqa: E402
 
 PEAK_HBM_GBPS = 8000.0
 METRIC = "candidate decode steps/s (attn+evict+entropy)"
 DEFAULT_EXTRA = ("base7b", "base72b_helper")
-KERNEL_SOURCES = ("attn.hip", "evict.hip", "entropy.hip", "kvr_device.h")
-
-
-def kernel_source_hash() -> str:
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2608_15797_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -131,14 +120,12 @@ def run_workload(name, steps, warmup, instrument=True):
     return res, dec, wl
 
 
-def copy_bandwidth(calibration=False, nbytes=1 << 30):
+def copy_bandwidth(nbytes=1 << 30):
     """Read+write bandwidth of a plain device-to-device copy of nbytes (a
-    measured reference beside the 8 TB/s nameplate). With calibration, the
-    copy runs three times so that profiler counters see a kernel of known
-    traffic (nbytes read, nbytes written per dispatch)."""
+    measured reference beside the 8 TB/s nameplate)."""
     src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
     dst = torch.empty_like(src)
-    reps = 3 if calibration else 5
+    reps = 5
     dst.copy_(src)
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -151,6 +138,20 @@ def copy_bandwidth(calibration=False, nbytes=1 << 30):
     del src, dst
     torch.cuda.empty_cache()
     return round(gbps, 1)
+
+
+def calibration_copy(nbytes=1 << 30):
+    """Three dispatches of a copy kernel of known traffic (nbytes read and
+    nbytes written each): a bf16 -> fp16 conversion, which runs as a kernel
+    (a same-type copy may go to a DMA engine that counters do not see). Profiler
+    byte counters on it calibrate those on the library's kernels."""
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty(nbytes // 2, dtype=torch.float16, device="cuda")
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def describe(wl):
@@ -166,16 +167,18 @@ def describe(wl):
     return d
 
 
-def traffic_for(name, kernel_key):
-    """HBM traffic of the dominant call measured by rocprofv3 PMC counters
-    (profiles/traffic_<workload>.json), if taken on the current kernels."""
+def traffic_for(name, call):
+    """HBM bytes per call of `call` measured with rocprofv3 PMC counters
+    (profiles/traffic_<workload>.json, written by profsum --traffic), or None
+    when the record is missing or was taken on other kernel sources."""
     path = os.path.join(ROOT, "profiles", "traffic_%s.json" % name)
     if not os.path.exists(path):
         return None
-    t = json.load(open(path))
-    if t.get("kernel_source_hash") != kernel_source_hash() or t.get("call") != kernel_key:
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("kernel_source_hash") != kernel_source_hash() or call not in t.get("calls", {}):
         return None
-    return t.get("bytes_per_call")
+    return t["calls"][call]["bytes_per_call"]
 
 
 def cpu_baseline(dec, wl, min_s=10.0):
@@ -254,8 +257,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-instrument", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="first run a plain 1 GiB device copy three times (reference for "
-                         "rocprofv3 FETCH_SIZE / WRITE_SIZE scaling)")
+                    help="first run a 1 GiB copy kernel three times (the known-size reference "
+                         "that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -264,7 +267,9 @@ def main():
         sys.exit(2)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    copy_ref = copy_bandwidth(calibration=args.copy_calibration)
+    if args.copy_calibration:
+        calibration_copy()
+    copy_ref = copy_bandwidth()
 
     res, dec, wl = run_workload(args.workload, args.steps, args.warmup, not args.no_instrument)
     steps = res["steps"]

@@ -212,6 +212,56 @@ int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, i
 
 size_t kvr_logit_entropy_workspace_size(int32_t R, int32_t V);
 
+/*
+ * kvr_fork -- batched copy of live KV slots between sequences: forking the N
+ * base candidates of a step from the persistent trajectory state, and
+ * retaining a selected base candidate as the new state (App. C, the fork-based
+ * best-of-(N+N) engine; Sec. 3.1 and Alg. 1: the selected base fork becomes
+ * the next base state).
+ *
+ *   src, dst : caches with equal L, Hkv, D and dtype; S and cap may differ.
+ *              They may describe the same cache: a row that is a source must
+ *              then be its own source (src_index[r] == r, a no-op), otherwise
+ *              what such a row passes on is unspecified.
+ *   src_index: [dst->S] int32 device: source sequence of each destination.
+ *              Destinations with an index outside [0, src->S) are skipped.
+ *   len      : [dst->S] int32 device: slots to copy, clamped to [0, min(src
+ *              cap, dst cap)]. For every (layer, KV head), slots [0, len[s])
+ *              of k, v (and pos when both caches track positions) move from
+ *              the source; slots beyond are untouched.
+ *   src_scores, dst_scores : NULL/NULL, or [S][L][Hkv][cap] float32 score rows
+ *              of the two caches, copied alongside (streamed window sums that a
+ *              fork inherits).
+ * Consecutive destinations (groups of 8) that share a source are served by
+ * one workgroup that reads the source once, so a source fanned out to N
+ * consecutive candidates is read from HBM once per group.
+ * Errors: KVR_EINVAL (shape or pointer mismatch, dst->pos without src->pos,
+ * one of the score pointers NULL), KVR_EUNSUPPORTED (dtype, D), KVR_EHIP.
+ */
+int kvr_fork(const kvr_cache *src, const kvr_cache *dst, const int32_t *src_index,
+             const int32_t *len, const float *src_scores, float *dst_scores,
+             hipStream_t stream);
+
+/*
+ * kvr_append -- bulk append of T tokens to every sequence: the base model
+ * encoding an accepted helper step in one forward pass (App. C; Alg. 1:
+ * append s_t to the base cache, then evict), or a prompt compressed in one
+ * shot. Score the appended window with kvr_accumulate_scores (nq = min(W, T))
+ * and evict with kvr_evict_topb afterwards.
+ *
+ *   len     : [S] int32 device, live length BEFORE the append (read only).
+ *   T       : tokens per sequence, T >= 0 (0: nothing is enqueued).
+ *   k_new, v_new : [S][L][Hkv][T][D] of the cache dtype; token i of
+ *             sequence s goes to slot len[s] + i of every (layer, KV head).
+ *   pos_new : NULL, or [S][T] int32 original positions, written to every
+ *             layer and head (needs cache->pos).
+ * Slots at or beyond cap are not written; the caller keeps len[s] + T <= cap.
+ * Errors: KVR_EINVAL (pointer, alignment, T < 0, pos_new without cache->pos),
+ * KVR_EUNSUPPORTED (dtype, D), KVR_EHIP.
+ */
+int kvr_append(const kvr_cache *cache, const int32_t *len, int32_t T, const void *k_new,
+               const void *v_new, const int32_t *pos_new, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

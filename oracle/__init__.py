@@ -132,6 +132,7 @@ def window_scores(K, V, n, q_win, scale):
     Hq, nq = q_win.shape[2], q_win.shape[3]
     assert q_win.shape == (S, L, Hq, nq, D)
     n = np.ascontiguousarray(np.broadcast_to(np.asarray(n, dtype=np.int32), (S,)))
+    assert (n >= 0).all() and (n <= cap).all()
     scores = np.zeros((S, L, Hkv, cap), np.float64)
     rc = lib().orc_window_scores(_p(K), _p(V), dt, S, L, Hkv, cap, D, _p(n), _p(q_win), Hq,
                                  nq, float(scale), _p(scores))

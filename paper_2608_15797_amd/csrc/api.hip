@@ -153,8 +153,13 @@ int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void
   if (st) return st;
   if (Hq <= 0 || nq <= 0) return fail(KVR_EINVAL, "Hq and nq must be positive");
   if (!len || !q_win || !scores) return fail(KVR_EINVAL, "len, q_win and scores are required");
-  const size_t lds = ((size_t)cache->D + 2 * (size_t)cache->cap) * sizeof(float);
+  const size_t lds = cache->dtype == KVR_BF16
+                        ? (size_t)cache->cap * sizeof(float)
+                        : ((size_t)cache->D + 2 * (size_t)cache->cap) * sizeof(float);
   if (lds > 65536) return fail(KVR_EUNSUPPORTED, "cap=%d needs too much LDS", cache->cap);
+  if (!aligned16(q_win)) return fail(KVR_EINVAL, "q_win not 16-byte aligned");
+  if ((double)G * nq * cache->D * 4 >= 2147483647.0)
+    return fail(KVR_EUNSUPPORTED, "window of %d rows is too large", G * nq);
   kvr::ScoreParams p{};
   p.k = cache->k; p.v = cache->v;
   p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.Hq = Hq; p.G = G;
@@ -180,6 +185,56 @@ int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scor
   p.dtype = cache->dtype; p.len = len; p.scores = scores;
   p.B = policy->B; p.W = policy->W; p.buffer = policy->buffer; p.kept = kept;
   return hip_status(kvr::launch_evict_topb(p, stream), "kvr_evict_topb launch");
+}
+
+int kvr_fork(const kvr_cache *src, const kvr_cache *dst, const int32_t *src_index,
+             const int32_t *len, const float *src_scores, float *dst_scores,
+             hipStream_t stream) {
+  int G = 0;
+  int st = check_cache(src, 0, &G);
+  if (st) return st;
+  st = check_cache(dst, 0, &G);
+  if (st) return st;
+  if (src->L != dst->L || src->Hkv != dst->Hkv || src->D != dst->D || src->dtype != dst->dtype)
+    return fail(KVR_EINVAL, "src and dst caches differ in L, Hkv, D or dtype");
+  if (!src_index || !len) return fail(KVR_EINVAL, "src_index and len are required");
+  if ((src_scores == nullptr) != (dst_scores == nullptr))
+    return fail(KVR_EINVAL, "src_scores and dst_scores must both be given or both be NULL");
+  if (dst->pos && !src->pos) return fail(KVR_EINVAL, "dst tracks positions but src does not");
+  const bool same = src->k == dst->k;
+  if (same && (src->v != dst->v || src->S != dst->S || src->cap != dst->cap ||
+               src->pos != dst->pos || src_scores != dst_scores))
+    return fail(KVR_EINVAL, "src and dst share k but are not the same cache");
+  if (!same && (src->v == dst->v))
+    return fail(KVR_EINVAL, "src and dst share v but not k");
+  kvr::ForkParams p{};
+  p.sk = src->k; p.sv = src->v; p.spos = dst->pos ? src->pos : nullptr; p.ssc = src_scores;
+  p.S_src = src->S; p.cap_src = src->cap;
+  p.dk = dst->k; p.dv = dst->v; p.dpos = dst->pos; p.dsc = dst_scores;
+  p.S_dst = dst->S; p.cap_dst = dst->cap;
+  p.L = dst->L; p.Hkv = dst->Hkv; p.D = dst->D; p.esz = dst->dtype == KVR_F32 ? 4 : 2;
+  p.same = same; p.src_index = src_index; p.len = len;
+  return hip_status(kvr::launch_fork(p, stream), "kvr_fork launch");
+}
+
+int kvr_append(const kvr_cache *cache, const int32_t *len, int32_t T, const void *k_new,
+               const void *v_new, const int32_t *pos_new, hipStream_t stream) {
+  int G = 0;
+  int st = check_cache(cache, 0, &G);
+  if (st) return st;
+  if (T < 0) return fail(KVR_EINVAL, "T=%d is negative", T);
+  if (pos_new && !cache->pos) return fail(KVR_EINVAL, "pos_new given but the cache has no pos");
+  if (T == 0) return KVR_OK;
+  if (!len || !k_new || !v_new) return fail(KVR_EINVAL, "len, k_new and v_new are required");
+  if (!aligned16(k_new) || !aligned16(v_new)) return fail(KVR_EINVAL, "k_new/v_new not 16-byte aligned");
+  const int esz = cache->dtype == KVR_F32 ? 4 : 2;
+  const long chunks = ((long)T * cache->D * esz / 16 + 1023) / 1024;
+  if (chunks > 65535) return fail(KVR_EUNSUPPORTED, "T=%d tokens per call is too many", T);
+  kvr::AppendParams p{};
+  p.k = cache->k; p.v = cache->v; p.pos = cache->pos;
+  p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.cap = cache->cap; p.D = cache->D;
+  p.esz = esz; p.len = len; p.T = T; p.k_new = k_new; p.v_new = v_new; p.pos_new = pos_new;
+  return hip_status(kvr::launch_append(p, stream), "kvr_append launch");
 }
 
 size_t kvr_logit_entropy_workspace_size(int32_t R, int32_t V) {

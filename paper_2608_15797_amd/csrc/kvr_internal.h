@@ -79,4 +79,30 @@ int entropy_splits(int R, int V);
 size_t entropy_workspace_bytes(int R, int V);
 hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream);
 
+struct ForkParams {
+  const void *sk, *sv;
+  const int32_t *spos;
+  const float *ssc;
+  int S_src, cap_src;
+  void *dk, *dv;
+  int32_t *dpos;
+  float *dsc;
+  int S_dst, cap_dst;
+  int L, Hkv, D, esz;
+  int same;  // src and dst are the same cache
+  const int32_t *src_index, *len;
+};
+hipError_t launch_fork(const ForkParams &p, hipStream_t stream);
+
+struct AppendParams {
+  void *k, *v;
+  int32_t *pos;
+  int S, L, Hkv, cap, D, esz;
+  const int32_t *len;
+  int T;
+  const void *k_new, *v_new;
+  const int32_t *pos_new;
+};
+hipError_t launch_append(const AppendParams &p, hipStream_t stream);
+
 }  // namespace kvr

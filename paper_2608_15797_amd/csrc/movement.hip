@@ -1,0 +1,174 @@
+// Data movement around the decode loop: forking candidates from a trajectory
+// state (or retaining a candidate as the state) and appending a step's tokens
+// in bulk (App. C, the fork-based engine; Alg. 1, retain / append-and-evict).
+//
+// Both are plain HBM copies of contiguous slot ranges: in the [cap][D] layout
+// of each (sequence, layer, KV head) the live slots [0, n) of K and of V are
+// one contiguous run of n * D elements, and an append writes one contiguous
+// run of T * D elements. Workgroups stream 16-byte vectors with all of a
+// round's loads issued before its stores.
+//
+// Fork: one workgroup per (group of kGroup consecutive destinations, layer,
+// KV head). Within a group, destinations that share a source form runs; each
+// round loads a chunk of the run's source once and stores it to every
+// destination of the run. Forking N candidates from one state (destinations
+// s*N .. s*N+N-1 reading source s) therefore reads each source byte from HBM
+// once, whatever the L2 does, and the stores stream at full rate.
+#include <hip/hip_runtime.h>
+
+#include "kvr_device.h"
+#include "kvr_internal.h"
+
+namespace kvr {
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+constexpr int kGroup = 8;
+
+// Loads one round (kUnroll vectors per thread) of a run's source rows.
+__device__ __forceinline__ void load_round(const u32x4 *__restrict__ src, int base, int nv,
+                                           u32x4 (&r)[kUnroll]) {
+#pragma unroll
+  for (int a = 0; a < kUnroll; a++) {
+    const int i = base + a * kThreads;
+    if (i < nv) r[a] = src[i];
+  }
+}
+
+__device__ __forceinline__ void store_round(u32x4 *__restrict__ dst, int base, int nv,
+                                            const u32x4 (&r)[kUnroll]) {
+#pragma unroll
+  for (int a = 0; a < kUnroll; a++) {
+    const int i = base + a * kThreads;
+    if (i < nv) dst[i] = r[a];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void fork_kernel(ForkParams p, int row_units) {
+  const int s0 = blockIdx.x * kGroup;
+  const int lh = blockIdx.y;  // l * Hkv + h
+  const int tid = threadIdx.x;
+  const int cmax = p.cap_src < p.cap_dst ? p.cap_src : p.cap_dst;
+  // Per destination of the group: source row (-1: skip) and slots to copy.
+  int src[kGroup], nn[kGroup];
+  int nvmax = 0;
+#pragma unroll
+  for (int j = 0; j < kGroup; j++) {
+    const int s = s0 + j;
+    int r = -1, n = 0;
+    if (s < p.S_dst) {
+      r = p.src_index[s];
+      n = p.len[s];
+      n = n < 0 ? 0 : (n > cmax ? cmax : n);
+      if (r < 0 || r >= p.S_src || (p.same && r == s) || n == 0) r = -1;
+    }
+    src[j] = r;
+    nn[j] = r < 0 ? 0 : n;
+    nvmax = max(nvmax, nn[j] * row_units);
+  }
+  const size_t row_vec = (size_t)row_units;
+  const size_t sstride = (size_t)p.L * p.Hkv;
+  for (int base = tid; base < nvmax; base += kUnroll * kThreads) {
+    int j = 0;
+    while (j < kGroup) {
+      const int r = src[j];
+      if (r < 0) {
+        j++;
+        continue;
+      }
+      // Run j .. e-1 shares source r; read as far as its longest member.
+      int e = j + 1, nvr = nn[j] * row_units;
+      while (e < kGroup && src[e] == r) {
+        nvr = max(nvr, nn[e] * row_units);
+        e++;
+      }
+      const size_t su = (size_t)r * sstride + lh;
+      u32x4 rk[kUnroll], rv[kUnroll];
+      load_round(static_cast<const u32x4 *>(p.sk) + su * p.cap_src * row_vec, base, nvr, rk);
+      load_round(static_cast<const u32x4 *>(p.sv) + su * p.cap_src * row_vec, base, nvr, rv);
+      for (int k = j; k < e; k++) {
+        const size_t du = (size_t)(s0 + k) * sstride + lh;
+        store_round(static_cast<u32x4 *>(p.dk) + du * p.cap_dst * row_vec, base, nn[k] * row_units, rk);
+        store_round(static_cast<u32x4 *>(p.dv) + du * p.cap_dst * row_vec, base, nn[k] * row_units, rv);
+      }
+      j = e;
+    }
+  }
+  if (p.dpos || p.dsc) {
+#pragma unroll
+    for (int j = 0; j < kGroup; j++) {
+      if (src[j] < 0) continue;
+      const size_t su = (size_t)src[j] * sstride + lh;
+      const size_t du = (size_t)(s0 + j) * sstride + lh;
+      for (int t = tid; t < nn[j]; t += kThreads) {
+        if (p.dpos) p.dpos[du * p.cap_dst + t] = p.spos[su * p.cap_src + t];
+        if (p.dsc) p.dsc[du * p.cap_dst + t] = p.ssc[su * p.cap_src + t];
+      }
+    }
+  }
+}
+
+// grid (units, chunks): chunk c of unit u copies vectors
+// [c * kUnroll * kThreads, (c + 1) * kUnroll * kThreads) of the unit's T rows.
+__global__ __launch_bounds__(kThreads) void append_kernel(AppendParams p, int row_units) {
+  const int unit = blockIdx.x;  // (s * L + l) * Hkv + h
+  const int s = unit / (p.L * p.Hkv);
+  int n = p.len[s];
+  n = n < 0 ? 0 : (n > p.cap ? p.cap : n);
+  const int rows = p.T < p.cap - n ? p.T : p.cap - n;  // rows that fit
+  const int nv = rows * row_units;
+  const int v0 = blockIdx.y * kUnroll * kThreads;
+  const int tid = threadIdx.x;
+  const size_t row_vec = (size_t)row_units;
+  const u32x4 *sk = static_cast<const u32x4 *>(p.k_new) + (size_t)unit * p.T * row_vec;
+  const u32x4 *sv = static_cast<const u32x4 *>(p.v_new) + (size_t)unit * p.T * row_vec;
+  u32x4 *dk = static_cast<u32x4 *>(p.k) + ((size_t)unit * p.cap + n) * row_vec;
+  u32x4 *dv = static_cast<u32x4 *>(p.v) + ((size_t)unit * p.cap + n) * row_vec;
+  u32x4 rk[kUnroll], rv[kUnroll];
+#pragma unroll
+  for (int a = 0; a < kUnroll; a++) {
+    const int i = v0 + tid + a * kThreads;
+    if (i < nv) {
+      rk[a] = sk[i];
+      rv[a] = sv[i];
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < kUnroll; a++) {
+    const int i = v0 + tid + a * kThreads;
+    if (i < nv) {
+      dk[i] = rk[a];
+      dv[i] = rv[a];
+    }
+  }
+  if (p.pos_new && blockIdx.y == 0) {
+    int32_t *dp = p.pos + (size_t)unit * p.cap + n;
+    const int32_t *sp = p.pos_new + (size_t)s * p.T;
+    for (int j = tid; j < rows; j += kThreads) dp[j] = sp[j];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_fork(const ForkParams &p, hipStream_t stream) {
+  const int row_units = p.D * p.esz / 16;
+  const dim3 grid((p.S_dst + kGroup - 1) / kGroup, p.L * p.Hkv);
+  hipLaunchKernelGGL(fork_kernel, grid, dim3(kThreads), 0, stream, p, row_units);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendParams &p, hipStream_t stream) {
+  const int row_units = p.D * p.esz / 16;
+  const long nv = (long)p.T * row_units;
+  const int chunks = (int)((nv + kUnroll * kThreads - 1) / (kUnroll * kThreads));
+  hipLaunchKernelGGL(append_kernel, dim3(p.S * p.L * p.Hkv, chunks), dim3(kThreads), 0, stream, p,
+                     row_units);
+  return hipGetLastError();
+}
+
+}  // namespace kvr

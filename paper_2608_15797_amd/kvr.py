@@ -24,7 +24,7 @@ STATUS = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_EUNSUPPORTED", -3: "KVR_EHIP",
 # Every symbol declared in include/kvr.h.
 EXPORTS = ("kvr_strerror", "kvr_last_error", "kvr_decode_attn", "kvr_decode_attn_workspace_size",
            "kvr_accumulate_scores", "kvr_evict_topb", "kvr_logit_entropy",
-           "kvr_logit_entropy_workspace_size")
+           "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append")
 
 
 class KvrError(RuntimeError):
@@ -78,6 +78,10 @@ def _load():
     lib.kvr_logit_entropy.restype = ctypes.c_int
     lib.kvr_logit_entropy_workspace_size.argtypes = [i32, i32]
     lib.kvr_logit_entropy_workspace_size.restype = sz
+    lib.kvr_fork.argtypes = [P(c_cache), P(c_cache), vp, vp, vp, vp, vp]
+    lib.kvr_fork.restype = ctypes.c_int
+    lib.kvr_append.argtypes = [P(c_cache), vp, i32, vp, vp, vp, vp]
+    lib.kvr_append.restype = ctypes.c_int
     return lib
 
 
@@ -245,3 +249,26 @@ def logit_entropy(logits: torch.Tensor, H: torch.Tensor, V: Optional[int] = None
                                0 if workspace is None else workspace.numel() * workspace.element_size(),
                                _stream(stream))
     _check(rc, "kvr_logit_entropy")
+
+
+def fork(src: Cache, dst: Cache, src_index: torch.Tensor, len_: torch.Tensor,
+         src_scores: Optional[torch.Tensor] = None, dst_scores: Optional[torch.Tensor] = None,
+         stream=None) -> None:
+    """kvr_fork: slots [0, len[s]) of sequence src_index[s] of src -> sequence s of dst."""
+    sc, dc = src.c(), dst.c()
+    for t in (src_index, len_, src_scores, dst_scores):
+        assert t is None or (t.is_contiguous() and t.is_cuda)
+    rc = lib.kvr_fork(ctypes.byref(sc), ctypes.byref(dc), _ptr(src_index), _ptr(len_),
+                      _ptr(src_scores), _ptr(dst_scores), _stream(stream))
+    _check(rc, "kvr_fork")
+
+
+def append(cache: Cache, len_: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+           pos_new: Optional[torch.Tensor] = None, stream=None) -> None:
+    """kvr_append: k_new, v_new [S][L][Hkv][T][D] to slots len[s] .. len[s]+T-1."""
+    cc = cache.c()
+    for t in (len_, k_new, v_new, pos_new):
+        assert t is None or t.is_contiguous()
+    rc = lib.kvr_append(ctypes.byref(cc), _ptr(len_), k_new.shape[3], _ptr(k_new), _ptr(v_new),
+                        _ptr(pos_new), _stream(stream))
+    _check(rc, "kvr_append")

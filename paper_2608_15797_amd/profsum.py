@@ -1,23 +1,80 @@
 """Summarise rocprofv3 result databases as short text.
 
     python -m paper_2608_15797_amd.profsum DIR [DIR ...]
+    python -m paper_2608_15797_amd.profsum --traffic OUT.json --workload NAME \
+        --calib-bytes N FETCH_DIR WRITE_DIR
 
-For every *_results.db under each DIR prints, per kernel, the dispatch count
-and average duration, and the per-dispatch average of every collected PMC
-counter (FETCH_SIZE / WRITE_SIZE in KiB). Kernels whose name contains "copy"
-are listed too: a plain copy of known size is the reference that scales the
-byte counters.
+The first form prints, for every *_results.db under each DIR, per kernel the
+dispatch count and average duration, and the per-dispatch average of every
+collected PMC counter (FETCH_SIZE / WRITE_SIZE in KiB). Kernels whose name
+contains "copy" are listed too, tagged "copy <name> grid=<grid size>".
+
+The second form turns one FETCH_SIZE pass and one WRITE_SIZE pass into HBM
+bytes per library call: each counter is scaled by the factor that maps its
+reading on a plain copy kernel of known size (N bytes read and N bytes
+written per dispatch; the copy whose WRITE_SIZE is within 10% of N) onto N,
+and the kernels that make up one call (CALL_KERNELS) are summed. The record
+carries a hash of the kernel sources so that a reader can tell whether it
+was taken on the kernels it runs.
 """
 from __future__ import annotations
 
+import argparse
 import collections
 import glob
+import hashlib
+import json
+import os
+import re
 import sqlite3
-import sys
+
+CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+KERNEL_SOURCES = ("attn.hip", "evict.hip", "entropy.hip", "kvr_device.h")
+
+# Kernels launched by one call of each hot-path entry point, by call name.
+CALL_KERNELS = {
+    "base_attn": (r"attn_cache_bf16<\d+, false",),
+    "helper_attn": (r"attn_prefix_bf16<", r"attn_cache_bf16<\d+, true"),
+    "evict": (r"evict_topb_kernel",),
+    "entropy": (r"entropy_kernel<", r"entropy_merge"),
+}
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def keep(name: str) -> bool:
     return "kvr" in name or "copy" in name.lower()
+
+
+def _dbs(d: str) -> list[str]:
+    return sorted(glob.glob(d + "/**/*_results.db", recursive=True))
+
+
+def counters(db: str) -> dict:
+    """{(tag, counter): (sum of values, dispatches)}; copies are tagged by grid."""
+    c = sqlite3.connect(db)
+    cols = [x[1] for x in c.execute("pragma table_info(counters_collection)")]
+    agg = collections.defaultdict(lambda: [0.0, 0])
+    if not cols:
+        return agg
+    for row in c.execute("select * from counters_collection"):
+        r = dict(zip(cols, row))
+        name = r.get("kernel_name") or ""
+        if not keep(name):
+            continue
+        tag = name
+        if "copy" in name.lower():
+            tag = "copy %s grid=%s" % (name[:50], r.get("grid_size", r.get("grid_x", "?")))
+        a = agg[(tag, r.get("counter_name"))]
+        a[0] += float(r.get("value") or 0.0)
+        a[1] += 1
+    return agg
 
 
 def summarise(db: str) -> list[str]:
@@ -27,33 +84,74 @@ def summarise(db: str) -> list[str]:
     for name, calls, avg in rows:
         if keep(name):
             out.append("duration  %-78s calls %7d  avg_us %10.2f" % (name[:78], calls, avg))
-    cols = [x[1] for x in c.execute("pragma table_info(counters_collection)")]
-    if cols:
-        # Copies are told apart by grid size (the calibration copy has its own).
-        agg = collections.defaultdict(lambda: [0.0, 0])
-        for row in c.execute("select * from counters_collection"):
-            r = dict(zip(cols, row))
-            name = r.get("kernel_name") or ""
-            if not keep(name):
-                continue
-            tag = name[:70]
-            if "copy" in name.lower():
-                tag = "%s grid=%s" % (name[:50], r.get("grid_size", r.get("grid_x", "?")))
-            a = agg[(tag, r.get("counter_name"))]
-            a[0] += float(r.get("value") or 0.0)
-            a[1] += 1
-        for (name, cn), (v, n) in sorted(agg.items()):
-            out.append("counter   %-78s %-24s avg %16.1f  (dispatches %d)" % (name, cn, v / n, n))
+    for (name, cn), (v, n) in sorted(counters(db).items()):
+        out.append("counter   %-78s %-24s avg %16.1f  (dispatches %d)" % (name[:78], cn, v / n, n))
     return out
 
 
-def main(argv):
-    for d in argv:
-        for db in sorted(glob.glob(d + "/**/*_results.db", recursive=True)):
+def _per_dispatch(dirs: list[str], counter: str) -> dict:
+    per = {}
+    for d in dirs:
+        for db in _dbs(d):
+            for (tag, cn), (v, n) in counters(db).items():
+                if cn == counter:
+                    per[tag] = (v / n, n)
+    return per
+
+
+def traffic(fetch_dir: str, write_dir: str, calib_bytes: int, workload: str) -> dict:
+    fetch = _per_dispatch([fetch_dir], "FETCH_SIZE")
+    write = _per_dispatch([write_dir], "WRITE_SIZE")
+    kib = calib_bytes / 1024.0
+    cal = [t for t in write if t.startswith("copy ") and abs(write[t][0] - kib) <= 0.1 * kib]
+    if len(cal) != 1 or cal[0] not in fetch:
+        raise SystemExit("no unique calibration copy of %d bytes among %s" % (calib_bytes, sorted(write)))
+    tag = cal[0]
+    f_read = calib_bytes / (fetch[tag][0] * 1024.0)
+    f_write = calib_bytes / (write[tag][0] * 1024.0)
+    calls = {}
+    for call, pats in CALL_KERNELS.items():
+        parts, rd, wr = [], 0.0, 0.0
+        for p in pats:
+            ks = [k for k in fetch if re.search(p, k) and k in write]
+            if len(ks) != 1:
+                break
+            k = ks[0]
+            parts.append(dict(kernel=k, dispatches=fetch[k][1],
+                              read_bytes=int(fetch[k][0] * 1024 * f_read),
+                              write_bytes=int(write[k][0] * 1024 * f_write)))
+            rd += parts[-1]["read_bytes"]
+            wr += parts[-1]["write_bytes"]
+        else:
+            calls[call] = dict(read_bytes=int(rd), write_bytes=int(wr), bytes_per_call=int(rd + wr),
+                               kernels=parts)
+    return dict(workload=workload, kernel_source_hash=kernel_source_hash(),
+                calibration=dict(kernel=tag, bytes=calib_bytes, fetch_factor=round(f_read, 4),
+                                 write_factor=round(f_write, 4)),
+                calls=calls)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("dirs", nargs="+")
+    ap.add_argument("--traffic", help="write the per-call traffic record to this JSON file")
+    ap.add_argument("--workload", default="")
+    ap.add_argument("--calib-bytes", type=int, default=1 << 30)
+    args = ap.parse_args(argv)
+    if args.traffic:
+        if len(args.dirs) != 2:
+            raise SystemExit("--traffic takes the FETCH_SIZE and the WRITE_SIZE result directories")
+        rec = traffic(args.dirs[0], args.dirs[1], args.calib_bytes, args.workload)
+        with open(args.traffic, "w") as fh:
+            json.dump(rec, fh, indent=1)
+        print(json.dumps(rec, indent=1))
+        return
+    for d in args.dirs:
+        for db in _dbs(d):
             print("##", db)
             for line in summarise(db):
                 print(line)
 
 
 if __name__ == "__main__":
-    main(sys.argv[1:])
+    main()

@@ -85,3 +85,34 @@ def test_prefix_workspace_size_matches_split_plan():
     n = kvr.lib.kvr_decode_attn_workspace_size(ctypes.byref(c), ctypes.byref(p), 12)
     rec = 128 * 28 * 12 * (128 + 4) * 4
     assert n % rec == 0 and n // rec >= 2
+
+
+def test_fork_rejects_bad_arguments_on_host():
+    from paper_2608_15797_amd import kvr
+    src = _cache(kvr)
+    cases = [
+        (_cache(kvr, k=48, v=64, L=2), 16, 16, None, None, "differ"),
+        (_cache(kvr, k=48, v=64, dtype=0), 16, 16, None, None, "differ"),
+        (_cache(kvr, k=48, v=64), None, 16, None, None, "required"),
+        (_cache(kvr, k=48, v=64), 16, 16, 16, None, "both"),
+        (_cache(kvr, k=48, v=64, pos=80), 16, 16, None, None, "positions"),
+        (_cache(kvr, k=16, v=64), 16, 16, None, None, "same cache"),
+        (_cache(kvr, k=48, v=16), 16, 16, None, None, "share v"),
+    ]
+    for dst, idx, ln, ssc, dsc, msg in cases:
+        rc = kvr.lib.kvr_fork(ctypes.byref(src), ctypes.byref(dst), idx, ln, ssc, dsc, None)
+        assert rc == -1, msg
+        assert msg in kvr.lib.kvr_last_error().decode()
+
+
+def test_append_rejects_bad_arguments_on_host():
+    from paper_2608_15797_amd import kvr
+    c = _cache(kvr)
+    assert kvr.lib.kvr_append(ctypes.byref(c), 16, -1, 16, 16, None, None) == -1
+    assert kvr.lib.kvr_append(ctypes.byref(c), 16, 3, 16, 16, 16, None) == -1   # no cache pos
+    assert "pos" in kvr.lib.kvr_last_error().decode()
+    assert kvr.lib.kvr_append(ctypes.byref(c), 16, 3, None, 16, None, None) == -1
+    assert kvr.lib.kvr_append(ctypes.byref(c), 16, 3, 24, 16, None, None) == -1  # alignment
+    assert kvr.lib.kvr_append(ctypes.byref(c), 16, 1 << 30, 16, 16, None, None) == -2
+    # T == 0 enqueues nothing and needs no token arrays
+    assert kvr.lib.kvr_append(ctypes.byref(c), 16, 0, None, None, None, None) == 0

@@ -331,17 +331,25 @@ def test_evict_topb_ties_and_gpu_scores_selection():
 
 # ------------------------------------------------------------ window scores
 
-@pytest.mark.parametrize("dt,D,G,nq", [(torch.float32, 64, 4, 8), (torch.bfloat16, 128, 7, 32),
-                                       (torch.bfloat16, 128, 8, 5)])
-def test_accumulate_scores(dt, D, G, nq):
+@pytest.mark.parametrize("dt,D,G,nq,cap", [
+    (torch.float32, 64, 4, 8, 97),
+    (torch.bfloat16, 128, 7, 32, 97),
+    (torch.bfloat16, 128, 8, 5, 97),
+    (torch.bfloat16, 64, 4, 8, 97),
+    (torch.bfloat16, 128, 16, 33, 130),    # 33 row blocks: the last pair is half empty
+    (torch.bfloat16, 128, 1, 3, 40),       # fewer rows than one block
+    (torch.bfloat16, 128, 7, 128, 300),    # a committed step's window on the 7B head shape
+])
+def test_accumulate_scores(dt, D, G, nq, cap):
     """kvr_accumulate_scores equals the oracle's causal window re-computation,
-    in both overwrite and accumulate modes."""
+    in both overwrite and accumulate modes; lengths include the full cache, a
+    ragged one, nq + 1 and fewer than nq (early window rows then see nothing)."""
     k = kvr()
-    S, L, Hkv, cap = 3, 2, 2, 97
+    S, L, Hkv = 4, 2, 2
     g = torch.Generator().manual_seed(D + G + nq)
     K = randn((S, L, Hkv, cap, D), g, dt)
     V = randn((S, L, Hkv, cap, D), g, dt)
-    lens = [cap, 50, nq + 1][:S]
+    lens = [cap, min(50, cap - 3), min(nq + 1, cap), max(1, min(nq - 2, cap))]
     qw = randn((S, L, Hkv * G, nq, D), g, dt)
     scale = 1.0 / math.sqrt(D)
     cache = k.Cache(K.to(DEV), V.to(DEV), None)
