@@ -31,7 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 from paper_2608_15797_amd import accounting as acc  # noqa: E402
-from paper_2608_15797_amd.profsum import kernel_source_hash  # noqa: E402
+from paper_2608_15797_amd.profsum import source_hash  # noqa: E402
 from paper_2608_15797_amd.workloads import WORKLOADS  # noqa: E402
 
 PEAK_HBM_GBPS = 8000.0
@@ -154,6 +154,41 @@ def calibration_copy(nbytes=1 << 30):
     torch.cuda.empty_cache()
 
 
+def sampler_cost(dec, wl, reps=50):
+    """Per-call time of the entropy pass alone and with the fused sampler
+    (temperature 0.8, top-k 20, top-p 0.95) on the workload's logit sets."""
+    from paper_2608_15797_amd import kvr
+    si = dec.inputs(dec.T_prompt)
+    out = {}
+    for w, (lg, ls) in enumerate(zip(si.logits, wl.logits)):
+        H = torch.empty(ls.R, device="cuda")
+        tok = torch.empty(ls.R, dtype=torch.int32, device="cuda")
+        smp = kvr.Sampler(seed=2608)
+        n = kvr.logit_entropy_sample_workspace_size(ls.R, ls.V, smp.top_k)
+        ws = torch.empty(max(n, 16) // 4 + 4, device="cuda")
+
+        def ent():
+            kvr.logit_entropy(lg, H, V=ls.V, workspace=dec.ews[w])
+
+        def ent_sample():
+            kvr.logit_entropy_sample(lg, H, tok, smp, V=ls.V, workspace=ws)
+
+        res = {}
+        for name, fn in (("entropy_us", ent), ("entropy_sample_us", ent_sample)):
+            fn()
+            torch.cuda.synchronize()
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            for _ in range(reps):
+                fn()
+            e.record()
+            torch.cuda.synchronize()
+            res[name] = round(s.elapsed_time(e) * 1e3 / reps, 2)
+        res["R"], res["V"] = ls.R, ls.V
+        out["logits%d" % w] = res
+    return out
+
+
 def describe(wl):
     d = {"workload": wl.name, "dtype": wl.dtype}
     if wl.base:
@@ -176,9 +211,10 @@ def traffic_for(name, call):
         return None
     with open(path) as fh:
         t = json.load(fh)
-    if t.get("kernel_source_hash") != kernel_source_hash() or call not in t.get("calls", {}):
+    rec = t.get("calls", {}).get(call)
+    if rec is None or rec.get("source_hash") != source_hash(call):
         return None
-    return t["calls"][call]["bytes_per_call"]
+    return rec["bytes_per_call"]
 
 
 def cpu_baseline(dec, wl, min_s=10.0):
@@ -281,6 +317,9 @@ def main():
         roof = dict(bound="hbm", achieved=c["GBps"], peak=PEAK_HBM_GBPS, unit="GB/s", frac=c["frac"],
                     traffic=traffic_for(args.workload, dom), call=dom,
                     alg_bytes_per_call=c["bytes_per_call"], avg_us=c["avg_us"])
+    sampler = sampler_cost(dec, wl) if not args.no_instrument else None
+    if sampler:
+        log("[%s] sampler: %s" % (args.workload, json.dumps(sampler)))
     cpu = None
     if not args.no_cpu_baseline:
         t0 = time.time()
@@ -307,6 +346,7 @@ def main():
         "ms_per_step": round(res["ms_per_step"], 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, Qwen2.5-Math shapes)",
         "config": cfg, "roofline": roof, "cpu_baseline": cpu, "workloads": extra,
+        "sampler": sampler,
         "copy_ref_GBps": copy_ref,
     }
     print(json.dumps(line), flush=True)

@@ -105,6 +105,24 @@ typedef struct kvr_detector {
     float tau;
 } kvr_detector;
 
+/* Token sampler fused with the entropy pass (Sec. 4.1 decoding setup:
+ * temperature 0.8, top-p 0.95, top-k 20).
+ *   temperature : > 0; probabilities are softmax(logits / temperature);
+ *   top_k       : 1 .. 64 candidates by logit, ties to the lower token id;
+ *   top_p       : (0, 1]; the shortest prefix of the top_k (by probability,
+ *                 renormalised over them) whose cumulative mass reaches top_p;
+ *   seed, step  : the draw for row r uses u = top 24 bits of the first word of
+ *                 Philox4x64-10 with counter (step, r, 0, 0) and key (seed, 0),
+ *                 divided by 2^24; the token is the first of the prefix whose
+ *                 cumulative mass exceeds u times the prefix mass. */
+typedef struct kvr_sampler {
+    float temperature;
+    int32_t top_k;
+    float top_p;
+    uint64_t seed;
+    uint64_t step;
+} kvr_sampler;
+
 /* Message for a status code (static storage). */
 const char *kvr_strerror(int status);
 
@@ -211,6 +229,25 @@ int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, i
                       size_t workspace_bytes, hipStream_t stream);
 
 size_t kvr_logit_entropy_workspace_size(int32_t R, int32_t V);
+
+/*
+ * kvr_logit_entropy_sample -- kvr_logit_entropy and the next token of every
+ * row from the same single pass over the logits (Eq. (4) entropy and the
+ * detector as there; sampling as described at kvr_sampler).
+ *
+ *   tokens    : [R] int32 output, the sampled token id of each row.
+ *   workspace : at least kvr_logit_entropy_sample_workspace_size(R, V, top_k)
+ *               bytes of device scratch, 16-byte aligned (no initialisation).
+ * Rows must hold at least one finite logit; NaN logits are not supported.
+ * Errors: as kvr_logit_entropy, plus KVR_EINVAL for sampler settings out of
+ * range.
+ */
+int kvr_logit_entropy_sample(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,
+                             float inv_temp, float *H, const kvr_detector *det,
+                             const kvr_sampler *sampler, int32_t *tokens, void *workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+size_t kvr_logit_entropy_sample_workspace_size(int32_t R, int32_t V, int32_t top_k);
 
 /*
  * kvr_fork -- batched copy of live KV slots between sequences: forking the N

@@ -242,30 +242,81 @@ size_t kvr_logit_entropy_workspace_size(int32_t R, int32_t V) {
   return kvr::entropy_workspace_bytes(R, V);
 }
 
-int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,
-                      float inv_temp, float *H, const kvr_detector *det, void *workspace,
-                      size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks shared by the entropy entry points; fills everything but splits/ws.
+int entropy_params(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,
+                   float inv_temp, float *H, const kvr_detector *det, kvr::EntropyParams *p) {
   if (!logits || !H) return fail(KVR_EINVAL, "logits and H are required");
   if (dtype != KVR_F32 && dtype != KVR_BF16) return fail(KVR_EUNSUPPORTED, "dtype %d", dtype);
   if (R <= 0 || V <= 0 || ld < V) return fail(KVR_EINVAL, "need R > 0, V > 0, ld >= V (R=%d V=%d ld=%ld)", R, V, (long)ld);
   if (R > 65535) return fail(KVR_EUNSUPPORTED, "R=%d rows exceeds 65535", R);
-  kvr::EntropyParams p{};
-  p.logits = logits; p.dtype = dtype; p.R = R; p.V = V; p.ld = ld; p.inv_temp = inv_temp; p.H = H;
+  *p = kvr::EntropyParams{};
+  p->logits = logits; p->dtype = dtype; p->R = R; p->V = V; p->ld = ld; p->inv_temp = inv_temp; p->H = H;
   if (det) {
     if (!det->hist || !det->cnt || !det->flag) return fail(KVR_EINVAL, "detector arrays are required");
     if (det->window <= 0 || det->guard < 0) return fail(KVR_EINVAL, "detector window must be positive");
-    p.hist = det->hist; p.cnt = det->cnt; p.flag = det->flag;
-    p.window = det->window; p.guard = det->guard; p.tau = det->tau;
+    p->hist = det->hist; p->cnt = det->cnt; p->flag = det->flag;
+    p->window = det->window; p->guard = det->guard; p->tau = det->tau;
   }
+  return KVR_OK;
+}
+
+int attach_workspace(kvr::EntropyParams *p, size_t need, void *workspace, size_t workspace_bytes) {
+  if (need == 0) return KVR_OK;
+  if (!workspace || workspace_bytes < need)
+    return fail(KVR_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  if (!aligned16(workspace)) return fail(KVR_EINVAL, "workspace not 16-byte aligned");
+  p->ws = workspace;
+  return KVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,
+                      float inv_temp, float *H, const kvr_detector *det, void *workspace,
+                      size_t workspace_bytes, hipStream_t stream) {
+  kvr::EntropyParams p;
+  int st = entropy_params(logits, dtype, R, V, ld, inv_temp, H, det, &p);
+  if (st) return st;
   p.splits = kvr::entropy_splits(R, V);
-  const size_t need = kvr::entropy_workspace_bytes(R, V);
-  if (need > 0) {
-    if (!workspace || workspace_bytes < need)
-      return fail(KVR_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
-    if (!aligned16(workspace)) return fail(KVR_EINVAL, "workspace not 16-byte aligned");
-    p.ws = workspace;
-  }
+  st = attach_workspace(&p, kvr::entropy_workspace_bytes(R, V), workspace, workspace_bytes);
+  if (st) return st;
   return hip_status(kvr::launch_logit_entropy(p, stream), "kvr_logit_entropy launch");
+}
+
+size_t kvr_logit_entropy_sample_workspace_size(int32_t R, int32_t V, int32_t top_k) {
+  if (R <= 0 || V <= 0 || top_k < 1 || top_k > kvr::kTopKMax) return 0;
+  return kvr::sample_workspace_bytes(R, V, top_k);
+}
+
+int kvr_logit_entropy_sample(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,
+                             float inv_temp, float *H, const kvr_detector *det,
+                             const kvr_sampler *sampler, int32_t *tokens, void *workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  kvr::EntropyParams p;
+  int st = entropy_params(logits, dtype, R, V, ld, inv_temp, H, det, &p);
+  if (st) return st;
+  if (!sampler || !tokens) return fail(KVR_EINVAL, "sampler and tokens are required");
+  if (!(sampler->temperature > 0.f)) return fail(KVR_EINVAL, "temperature must be positive");
+  if (sampler->top_k < 1 || sampler->top_k > kvr::kTopKMax)
+    return fail(KVR_EINVAL, "top_k=%d is outside 1..%d", sampler->top_k, kvr::kTopKMax);
+  if (!(sampler->top_p > 0.f && sampler->top_p <= 1.f))
+    return fail(KVR_EINVAL, "top_p must lie in (0, 1]");
+  p.top_k = sampler->top_k;
+  p.inv_t = 1.0f / sampler->temperature;
+  p.top_p = sampler->top_p;
+  p.seed = sampler->seed;
+  p.step = sampler->step;
+  p.tokens = tokens;
+  p.splits = kvr::sample_splits(R, V, sampler->top_k);
+  st = attach_workspace(&p, kvr::sample_workspace_bytes(R, V, sampler->top_k), workspace, workspace_bytes);
+  if (st) return st;
+  return hip_status(kvr::launch_logit_entropy(p, stream), "kvr_logit_entropy_sample launch");
 }
 
 }  // extern "C"

@@ -18,6 +18,23 @@
 // past the split's range return zero without touching memory), issued U at a
 // time before any arithmetic, with invalid values masked by selects rather
 // than branches.
+//
+// Fused sampler (temperature, top-k, top-p; Sec. 4.1 decoding setup) in the
+// same pass. Each wave keeps its best candidates in LDS as 64-bit keys (an
+// order-preserving map of the raw logit's bits above the complemented token
+// id, so a larger key is a larger logit and, among equal logits, a lower id).
+// A candidate must beat the wave's threshold, the k-th best key at its last
+// compaction (seeded, in the first round, with the k-th largest of the lanes'
+// maxima, which bounds the wave's k-th best logit from below); a batch of 8
+// logits per lane in which no lane reaches it costs a few compares and one
+// vote. When the buffer would overflow, the wave keeps at most 128 of its best
+// and raises the threshold. Thresholds are found bit by bit from the top with
+// ballot counts only (compare, ballot, popcount; no cross-lane data movement),
+// stopping as soon as the kept count fits. Each split ends
+// with its k best keys in the workspace; the per-row merge takes the k best
+// of all splits, forms the temperature softmax over them, cuts the nucleus at
+// top_p and draws with a Philox4x64-10 uniform (counter (step, row, 0, 0),
+// key (seed, 0), top 24 bits of the first word).
 #include <hip/hip_runtime.h>
 
 #include "kvr_device.h"
@@ -121,21 +138,215 @@ __device__ void detector_push(const EntropyParams &p, int row, float H) {
   }
 }
 
+// ---------------------------------------------------------------- sampler
+
+__device__ __forceinline__ uint32_t order_bits(float x) {
+  const uint32_t u = x == 0.f ? 0u : __float_as_uint(x);  // -0 ranks as +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float from_order_bits(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+// Larger key = larger logit, then lower id. Every real key is > 0.
+__device__ __forceinline__ uint64_t cand_key(float x, uint32_t id) {
+  return ((uint64_t)order_bits(x) << 32) | (uint64_t)(~id);
+}
+
+constexpr int kKeep = 128;                        // entries kept by a compaction, at most
+constexpr int kCandCap = kKeep + kWave;           // wave buffer: one offer adds <= 64
+constexpr int kCandPerLane = kCandCap / kWave;    // 3
+
+// Wave-wide count of entries >= t (entries are keys, 0 = empty; t >= 1).
+template <int NPL>
+__device__ __forceinline__ int wave_count_ge(const uint64_t (&v)[NPL], uint64_t t) {
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < NPL; i++) c += __popcll(__ballot(v[i] >= t));
+  return c;
+}
+
+// A threshold t with k <= count(entries >= t) <= cap, built bit by bit from
+// the top with ballot counts only and stopped as soon as the count fits (with
+// cap = k: exactly the k largest keys, as keys are unique). Returns 1 when
+// all entries already fit.
+template <int NPL>
+__device__ __forceinline__ uint64_t select_threshold(const uint64_t (&v)[NPL], int k, int cap) {
+  if (wave_count_ge(v, 1) <= cap) return 1;
+  uint64_t t = 0;
+  for (int b = 63; b >= 0; b--) {
+    const uint64_t c = t | (1ull << b);
+    const int n = wave_count_ge(v, c);
+    if (n >= k) {
+      t = c;
+      if (n <= cap) break;
+    }
+  }
+  return t;
+}
+
+// Stores the wave's keys >= t to out[0 ..) (unordered); returns how many.
+template <int NPL>
+__device__ __forceinline__ int wave_store_ge(uint64_t *out, const uint64_t (&v)[NPL], uint64_t t, int lane) {
+  const uint64_t below = (1ull << lane) - 1ull;
+  int base = 0;
+#pragma unroll
+  for (int i = 0; i < NPL; i++) {
+    const bool m = v[i] >= t;
+    const uint64_t b = __ballot(m);
+    if (m) out[base + __popcll(b & below)] = v[i];
+    base += __popcll(b);
+  }
+  return base;
+}
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// A wave's candidate buffer: keys >= kmin are kept; logits below vmin cannot
+// reach kmin (vmin is the logit part of kmin).
+struct Cands {
+  uint64_t *buf;
+  int cnt;
+  uint64_t kmin;
+  float vmin;
+};
+
+// Keeps between k and cap of the buffered keys (cap = k: exactly the k best),
+// unordered in slots 0.., and raises the thresholds. NPL * 64 >= c.cnt.
+template <int NPL>
+__device__ __forceinline__ void cand_reduce(Cands &c, int k, int cap, int lane) {
+  wave_lds_sync();
+  uint64_t v[NPL];
+#pragma unroll
+  for (int i = 0; i < NPL; i++) {
+    const int j = lane + i * kWave;
+    v[i] = j < c.cnt ? c.buf[j] : 0;
+  }
+  const uint64_t t = select_threshold<NPL>(v, k, cap);
+  wave_lds_sync();
+  c.cnt = wave_store_ge<NPL>(c.buf, v, t, lane);
+  if (t > c.kmin) {
+    c.kmin = t;
+    c.vmin = from_order_bits((uint32_t)(t >> 32));
+  }
+  wave_lds_sync();
+}
+
+__device__ __forceinline__ void cand_reduce_any(Cands &c, int k, int cap, int lane) {
+  if (c.cnt <= kWave) cand_reduce<1>(c, k, cap, lane);
+  else if (c.cnt <= 2 * kWave) cand_reduce<2>(c, k, cap, lane);
+  else cand_reduce<kCandPerLane>(c, k, cap, lane);
+}
+
+// Buffer overflow (rare once the thresholds are seeded): keep at most kKeep.
+__device__ __forceinline__ void cand_compact(Cands &c, int k, int lane) {
+  cand_reduce<kCandPerLane>(c, k, kKeep, lane);
+}
+
+// Initial thresholds from the first round: the k-th largest of the lanes'
+// maxima (each an actual logit), so at least k of the wave's logits are at or
+// above it and nothing below it can be among the wave's k best.
+__device__ __forceinline__ void cand_seed(Cands &c, float lane_max, int k) {
+  const uint32_t ob = order_bits(lane_max);
+  const bool ok = lane_max > kNegInf;
+  if (__popcll(__ballot(ok)) < k) return;
+  uint32_t t = 0;
+  for (int b = 31; b >= 0; b--) {
+    const uint32_t cb = t | (1u << b);
+    if (__popcll(__ballot(ok && ob >= cb)) >= k) t = cb;
+  }
+  c.kmin = (uint64_t)t << 32;
+  c.vmin = from_order_bits(t);
+}
+
+// Offers up to 8 logits per lane (elements e < nvalid, ids id0 + e). Only
+// logits at or above vmin are looked at, one per lane per iteration.
+__device__ __forceinline__ void cand_offer(Cands &c, int k, int lane, const float (&x)[8], uint32_t id0,
+                                           int nvalid) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int e = 0; e < 8; e++) m |= ((e < nvalid) & (x[e] >= c.vmin)) ? (1u << e) : 0u;
+  const uint64_t below = (1ull << lane) - 1ull;
+  while (__any(m != 0)) {
+    const int e = m ? __builtin_ctz(m) : 0;
+    float xv = x[0];
+#pragma unroll
+    for (int q = 1; q < 8; q++) xv = e == q ? x[q] : xv;
+    const uint64_t key = m ? cand_key(xv, id0 + (uint32_t)e) : 0;
+    bool take = key != 0 && key >= c.kmin;
+    uint64_t b = __ballot(take);
+    if (c.cnt + __popcll(b) > kCandCap) {
+      cand_compact(c, k, lane);
+      take = key != 0 && key >= c.kmin;
+      b = __ballot(take);
+    }
+    if (take) c.buf[c.cnt + __popcll(b & below)] = key;
+    c.cnt += __popcll(b);
+    m &= m - 1u;
+  }
+}
+
+// Philox4x64-10 (Salmon et al., SC 2011): first output word.
+__device__ __forceinline__ uint64_t philox_w0(uint64_t c0, uint64_t c1, uint64_t k0, uint64_t k1) {
+  uint64_t c2 = 0, c3 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; r++) {
+    const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
+    const uint64_t lo0 = m0 * c0, hi0 = __umul64hi(m0, c0);
+    const uint64_t lo1 = m1 * c2, hi1 = __umul64hi(m1, c2);
+    const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+    k0 += 0x9E3779B97F4A7C15ull;
+    k1 += 0xBB67AE8584CAA73Bull;
+  }
+  return c0;
+}
+
+// The k best keys of the waves' candidate lists (wave w holds off[w+1]-off[w]
+// keys at cand[w * kCandCap ..]) stored unordered to out; returns how many.
+template <int NPL, int NW>
+__device__ __forceinline__ int gather_select(const uint64_t *cand, const int (&off)[NW + 1], int k, int lane,
+                                             uint64_t *out) {
+  uint64_t v[NPL];
+#pragma unroll
+  for (int i = 0; i < NPL; i++) {
+    const int j = lane + i * kWave;  // entry j of the concatenated lists
+    int w = 0;
+#pragma unroll
+    for (int q = 1; q < NW; q++) w += j >= off[q];
+    v[i] = j < off[NW] ? cand[w * kCandCap + (j - off[w])] : 0;
+  }
+  const uint64_t thr = select_threshold<NPL>(v, k, k);
+  return wave_store_ge<NPL>(out, v, thr, lane);
+}
+
 // VEC = true: 16-byte loads of 8 elements (row starts 16-byte aligned).
-template <typename T, bool VEC>
+// SAMPLE = true: also collect the split's top_k candidates (always writes
+// the split's partials, even unsplit rows, for the sampling merge).
+template <typename T, bool VEC, bool SAMPLE>
 __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
   __shared__ Tri part[kThreads / kWave];
+  __shared__ uint64_t cand[SAMPLE ? (kThreads / kWave) * kCandCap : 1];
+  __shared__ int cand_n[kThreads / kWave];
   const int row = blockIdx.y;
   const int split = blockIdx.x;
   const int splits = gridDim.x;
   const int tid = threadIdx.x;
+  const int lane = tid % kWave;
+  const int wave = tid / kWave;
   const T *x = static_cast<const T *>(p.logits) + (size_t)row * p.ld;
   const float c = p.inv_temp * kLog2e;
+  Cands cs{cand + (SAMPLE ? wave * kCandCap : 0), 0, 1, kNegInf};
 
   Tri t{kNegInf, 0.f, 0.f};
   if constexpr (VEC) {
     // U vectors of 8 logits per thread per round, all loads issued first.
-    constexpr int U = 8;
+    // Entropy alone: 10, so that a split of the 7B / 1.5B vocabularies over 8
+    // workgroups per row is one round (measured 22% faster than 8). With the
+    // sampler: 8, whose lower register count keeps 4 waves per SIMD.
+    constexpr int U = SAMPLE ? 8 : 10;
     const int nvec = p.V / 8;
     const int per = (nvec + splits - 1) / splits;
     const int v0 = split * per;
@@ -143,10 +354,32 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
     // The resource ends where this split's vectors end, so the lanes of a
     // partly used round load nothing instead of fetching the next split.
     const rsrc_t rr = row_rsrc(x, (uint32_t)v1 * 8u * (uint32_t)sizeof(T));
-    for (int base = v0 + tid; base < v1; base += U * kThreads) {
+    // The loop bound is the same for every thread (lanes past the end load
+    // zeros and mask them), so waves offer sampler candidates in lockstep.
+    for (int b0 = v0; b0 < v1; b0 += U * kThreads) {
+      const int base = b0 + tid;
       float y[U][8];
 #pragma unroll
-      for (int u = 0; u < U; u++) load8(rr, base + u * kThreads, c, y[u], x);
+      for (int u = 0; u < U; u++) load8(rr, base + u * kThreads, SAMPLE ? 1.0f : c, y[u], x);
+      if constexpr (SAMPLE) {
+        if (b0 == v0) {
+          // First round: seed the thresholds from the lanes' maxima.
+          float mx = kNegInf;
+#pragma unroll
+          for (int u = 0; u < U; u++)
+            if (base + u * kThreads < v1)
+#pragma unroll
+              for (int e = 0; e < 8; e++) mx = fmaxf(mx, y[u][e]);
+          cand_seed(cs, mx, p.top_k);
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+          const int v = base + u * kThreads;
+          cand_offer(cs, p.top_k, lane, y[u], (uint32_t)v * 8u, v < v1 ? 8 : 0);
+#pragma unroll
+          for (int e = 0; e < 8; e++) y[u][e] *= c;
+        }
+      }
 #pragma unroll
       for (int u = 0; u < U; u++) {
         const bool ok = base + u * kThreads < v1;
@@ -177,19 +410,35 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
         }
     }
     if (split == splits - 1) {
+      // The V % 8 trailing logits (one per thread of the first wave).
       const int e = nvec * 8 + tid;
-      if (e < p.V) {
-        float a[1] = {load1(x + e) * c};
-        tri_add<1>(t, a);
+      float a[8] = {kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf};
+      const bool has = e < p.V;
+      if (has) a[0] = load1(x + e);
+      if constexpr (SAMPLE) {
+        if (wave == 0) cand_offer(cs, p.top_k, lane, a, (uint32_t)e, has ? 1 : 0);
+      }
+      if (has) {
+        float b[1] = {a[0] * c};
+        tri_add<1>(t, b);
       }
     }
   } else {
     const int per = (p.V + splits - 1) / splits;
     const int e0 = split * per;
     const int e1 = min(e0 + per, p.V);
-    for (int e = e0 + tid; e < e1; e += kThreads) {
-      float a[1] = {load1(x + e) * c};
-      tri_add<1>(t, a);
+    // Every thread runs the same number of iterations so that whole waves
+    // offer candidates together.
+    for (int eb = e0; eb < e1; eb += kThreads) {
+      const int e = eb + tid;
+      const bool has = e < e1;
+      float a[8] = {kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf};
+      if (has) a[0] = load1(x + e);
+      if constexpr (SAMPLE) cand_offer(cs, p.top_k, lane, a, (uint32_t)e, has ? 1 : 0);
+      if (has) {
+        float b[1] = {a[0] * c};
+        tri_add<1>(t, b);
+      }
     }
   }
 
@@ -198,23 +447,53 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
     Tri o{shfl_xor(t.m, msk), shfl_xor(t.z, msk), shfl_xor(t.s, msk)};
     t = tri_merge(t, o);
   }
-  if ((tid & (kWave - 1)) == 0) part[tid / kWave] = t;
-  __syncthreads();
-  if (tid != 0) return;
-  Tri r = part[0];
-#pragma unroll
-  for (int w = 1; w < kThreads / kWave; w++) r = tri_merge(r, part[w]);
-
-  if (splits == 1) {
-    const float H = finish_entropy(r);
-    p.H[row] = H;
-    detector_push(p, row, H);
-    return;
+  if (lane == 0) part[wave] = t;
+  if constexpr (SAMPLE) {
+    if (cs.cnt > p.top_k) cand_reduce_any(cs, p.top_k, p.top_k, lane);  // exactly the k best
+    if (lane == 0) cand_n[wave] = cs.cnt;
   }
-  float *mine = static_cast<float *>(p.ws) + ((size_t)row * splits + split) * 4;
-  mine[0] = r.m;
-  mine[1] = r.z;
-  mine[2] = r.s;
+  __syncthreads();
+  if constexpr (SAMPLE) {
+    // First wave: the k best of the waves' lists go to the workspace.
+    if (wave != 0) return;
+    constexpr int NW = kThreads / kWave;
+    int off[NW + 1];
+    off[0] = 0;
+#pragma unroll
+    for (int w = 0; w < NW; w++) off[w + 1] = off[w] + cand_n[w];
+    uint64_t *keys = reinterpret_cast<uint64_t *>(static_cast<float *>(p.ws) + (size_t)p.R * splits * 4) +
+                     ((size_t)row * splits + split) * p.top_k;
+    int nw;
+    if (off[NW] <= kWave) nw = gather_select<1, NW>(cand, off, p.top_k, lane, keys);
+    else if (off[NW] <= 2 * kWave) nw = gather_select<2, NW>(cand, off, p.top_k, lane, keys);
+    else nw = gather_select<NW * kTopKMax / kWave, NW>(cand, off, p.top_k, lane, keys);
+    for (int q = nw + lane; q < p.top_k; q += kWave) keys[q] = 0;
+    if (lane == 0) {
+      Tri r = part[0];
+#pragma unroll
+      for (int w = 1; w < NW; w++) r = tri_merge(r, part[w]);
+      float *mine_t = static_cast<float *>(p.ws) + ((size_t)row * splits + split) * 4;
+      mine_t[0] = r.m;
+      mine_t[1] = r.z;
+      mine_t[2] = r.s;
+    }
+    return;
+  } else {
+    if (tid != 0) return;
+    Tri r = part[0];
+#pragma unroll
+    for (int w = 1; w < kThreads / kWave; w++) r = tri_merge(r, part[w]);
+    if (splits == 1) {
+      const float H = finish_entropy(r);
+      p.H[row] = H;
+      detector_push(p, row, H);
+      return;
+    }
+    float *mine = static_cast<float *>(p.ws) + ((size_t)row * splits + split) * 4;
+    mine[0] = r.m;
+    mine[1] = r.z;
+    mine[2] = r.s;
+  }
 }
 
 // Per-row merge of the split partials, then the detector; one thread per row.
@@ -227,6 +506,83 @@ __global__ __launch_bounds__(256) void entropy_merge(EntropyParams p) {
   const float H = finish_entropy(acc);
   p.H[row] = H;
   detector_push(p, row, H);
+}
+
+constexpr int kMergeEntries = 1024;  // splits * top_k bound of the sampling merge
+
+// Per-row sampling merge: one wave per row. Entropy and detector as in
+// entropy_merge; then the top_k best keys of all splits, the temperature
+// softmax over them, the top_p nucleus and the Philox draw. NPL * 64 >=
+// splits * top_k.
+template <int NPL>
+__global__ __launch_bounds__(kWave) void sample_merge(EntropyParams p) {
+  const int row = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int S = p.splits, K = p.top_k;
+  const float *q = static_cast<const float *>(p.ws) + (size_t)row * S * 4;
+  Tri acc{kNegInf, 0.f, 0.f};
+  for (int k = lane; k < S; k += kWave) acc = tri_merge(acc, Tri{q[4 * k], q[4 * k + 1], q[4 * k + 2]});
+#pragma unroll
+  for (int msk = 32; msk >= 1; msk >>= 1) {
+    Tri o{shfl_xor(acc.m, msk), shfl_xor(acc.z, msk), shfl_xor(acc.s, msk)};
+    acc = tri_merge(acc, o);
+  }
+  if (lane == 0) {
+    const float H = finish_entropy(acc);
+    p.H[row] = H;
+    detector_push(p, row, H);
+  }
+  // Candidates.
+  const uint64_t *keys = reinterpret_cast<const uint64_t *>(static_cast<const float *>(p.ws) +
+                                                            (size_t)p.R * S * 4) + (size_t)row * S * K;
+  const int E = S * K;
+  uint64_t v[NPL];
+#pragma unroll
+  for (int i = 0; i < NPL; i++) {
+    const int j = lane + i * kWave;
+    v[i] = j < E ? keys[j] : 0;
+  }
+  // The K best keys of all splits, then sorted (descending) by rank counting.
+  __shared__ uint64_t win[kTopKMax], sorted[kTopKMax];
+  const uint64_t thr = select_threshold<NPL>(v, K, K);
+  const int nwin = wave_store_ge<NPL>(win, v, thr, lane);
+  __syncthreads();
+  const uint64_t key = lane < nwin ? win[lane] : 0;
+  int rank = 0;
+  for (int j = 0; j < nwin; j++) rank += win[j] > key;
+  if (lane < nwin) sorted[rank] = key;
+  __syncthreads();
+  const uint64_t mine = lane < nwin ? sorted[lane] : 0;
+  const bool live = mine != 0;  // lanes 0 .. nwin - 1
+  const float xr = live ? from_order_bits((uint32_t)(mine >> 32)) : kNegInf;
+  const uint32_t id = ~(uint32_t)(mine & 0xffffffffu);
+  const float x0 = __shfl(xr, 0, kWave);
+  const float cexp = p.inv_t * kLog2e;
+  float e = live ? fast_exp2((xr - x0) * cexp) : 0.f;
+  if (!(e >= 0.f)) e = 0.f;  // -inf - (-inf) and similar never reach a live lane; belt and braces
+  // Inclusive prefix sum over lanes.
+  float cum = e;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const float o = __shfl_up(cum, off, kWave);
+    if (lane >= off) cum += o;
+  }
+  const uint64_t livemask = __ballot(live);
+  const int nlive = __popcll(livemask);
+  const float Z = __shfl(cum, nlive - 1, kWave);
+  int keep = nlive;
+  if (p.top_p < 1.0f) {
+    const uint64_t reach = __ballot(live && cum >= p.top_p * Z);
+    if (reach) keep = __ffsll((long long)reach);  // lowest lane + 1
+  }
+  const float mass = __shfl(cum, keep - 1, kWave);
+  const uint64_t w0 = philox_w0(p.step, (uint64_t)row, p.seed, 0);
+  const float u = (float)(w0 >> 40) * (1.0f / 16777216.0f);
+  const float target = u * mass;
+  const uint64_t over = __ballot(lane < keep && cum > target);
+  const int pick = over ? __ffsll((long long)over) - 1 : keep - 1;
+  const uint32_t tok = __shfl(id, pick, kWave);
+  if (lane == 0) p.tokens[row] = (int32_t)tok;
 }
 
 }  // namespace
@@ -249,19 +605,46 @@ size_t entropy_workspace_bytes(int R, int V) {
   return (size_t)R * s * 4 * sizeof(float);
 }
 
+int sample_splits(int R, int V, int top_k) {
+  int s = entropy_splits(R, V);
+  const int maxs = kMergeEntries / (top_k > 0 ? top_k : 1);
+  return s < maxs ? s : maxs;
+}
+
+size_t sample_workspace_bytes(int R, int V, int top_k) {
+  const int s = sample_splits(R, V, top_k);
+  return (size_t)R * s * 4 * sizeof(float) + (size_t)R * s * top_k * sizeof(uint64_t);
+}
+
+template <typename T, bool VEC>
+static void launch_split(const EntropyParams &p, dim3 grid, hipStream_t stream) {
+  if (p.top_k > 0) hipLaunchKernelGGL((entropy_kernel<T, VEC, true>), grid, dim3(kThreads), 0, stream, p);
+  else hipLaunchKernelGGL((entropy_kernel<T, VEC, false>), grid, dim3(kThreads), 0, stream, p);
+}
+
 hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream) {
   const dim3 grid(p.splits, p.R);
   const size_t esz = p.dtype == 0 ? 4 : 2;
   const bool vec = ((uintptr_t)p.logits % 16 == 0) && ((size_t)p.ld * esz % 16 == 0);
   if (p.dtype == 0) {
-    if (vec) hipLaunchKernelGGL((entropy_kernel<float, true>), grid, dim3(kThreads), 0, stream, p);
-    else hipLaunchKernelGGL((entropy_kernel<float, false>), grid, dim3(kThreads), 0, stream, p);
+    if (vec) launch_split<float, true>(p, grid, stream);
+    else launch_split<float, false>(p, grid, stream);
   } else {
-    if (vec) hipLaunchKernelGGL((entropy_kernel<bf16_t, true>), grid, dim3(kThreads), 0, stream, p);
-    else hipLaunchKernelGGL((entropy_kernel<bf16_t, false>), grid, dim3(kThreads), 0, stream, p);
+    if (vec) launch_split<bf16_t, true>(p, grid, stream);
+    else launch_split<bf16_t, false>(p, grid, stream);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.splits == 1) return e;
+  if (e != hipSuccess) return e;
+  if (p.top_k > 0) {
+    const int E = p.splits * p.top_k;
+    if (E <= 64) hipLaunchKernelGGL(sample_merge<1>, dim3(p.R), dim3(kWave), 0, stream, p);
+    else if (E <= 128) hipLaunchKernelGGL(sample_merge<2>, dim3(p.R), dim3(kWave), 0, stream, p);
+    else if (E <= 256) hipLaunchKernelGGL(sample_merge<4>, dim3(p.R), dim3(kWave), 0, stream, p);
+    else if (E <= 512) hipLaunchKernelGGL(sample_merge<8>, dim3(p.R), dim3(kWave), 0, stream, p);
+    else hipLaunchKernelGGL(sample_merge<16>, dim3(p.R), dim3(kWave), 0, stream, p);
+    return hipGetLastError();
+  }
+  if (p.splits == 1) return e;
   hipLaunchKernelGGL(entropy_merge, dim3((p.R + 255) / 256), dim3(256), 0, stream, p);
   return hipGetLastError();
 }

@@ -74,9 +74,19 @@ struct EntropyParams {
   float tau;
   void *ws;
   int splits;
+  // Fused sampler (top_k > 0): temperature, top-k, top-p and a Philox draw
+  // keyed by (seed, step, row); tokens [R] receive the sampled ids.
+  int top_k;
+  float inv_t;  // 1 / temperature
+  float top_p;
+  uint64_t seed, step;
+  int32_t *tokens;
 };
 int entropy_splits(int R, int V);
 size_t entropy_workspace_bytes(int R, int V);
+int sample_splits(int R, int V, int top_k);
+size_t sample_workspace_bytes(int R, int V, int top_k);
+constexpr int kTopKMax = 64;
 hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream);
 
 struct ForkParams {

@@ -24,7 +24,8 @@ STATUS = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_EUNSUPPORTED", -3: "KVR_EHIP",
 # Every symbol declared in include/kvr.h.
 EXPORTS = ("kvr_strerror", "kvr_last_error", "kvr_decode_attn", "kvr_decode_attn_workspace_size",
            "kvr_accumulate_scores", "kvr_evict_topb", "kvr_logit_entropy",
-           "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append")
+           "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append",
+           "kvr_logit_entropy_sample", "kvr_logit_entropy_sample_workspace_size")
 
 
 class KvrError(RuntimeError):
@@ -53,6 +54,11 @@ class c_detector(ctypes.Structure):
                 ("window", ctypes.c_int32), ("guard", ctypes.c_int32), ("tau", ctypes.c_float)]
 
 
+class c_sampler(ctypes.Structure):
+    _fields_ = [("temperature", ctypes.c_float), ("top_k", ctypes.c_int32), ("top_p", ctypes.c_float),
+                ("seed", ctypes.c_uint64), ("step", ctypes.c_uint64)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError("libkvr.so not built: run `python -m paper_2608_15797_amd.build` "
@@ -78,6 +84,11 @@ def _load():
     lib.kvr_logit_entropy.restype = ctypes.c_int
     lib.kvr_logit_entropy_workspace_size.argtypes = [i32, i32]
     lib.kvr_logit_entropy_workspace_size.restype = sz
+    lib.kvr_logit_entropy_sample.argtypes = [vp, i32, i32, i32, i64, f32, vp, P(c_detector),
+                                             P(c_sampler), vp, vp, sz, vp]
+    lib.kvr_logit_entropy_sample.restype = ctypes.c_int
+    lib.kvr_logit_entropy_sample_workspace_size.argtypes = [i32, i32, i32]
+    lib.kvr_logit_entropy_sample_workspace_size.restype = sz
     lib.kvr_fork.argtypes = [P(c_cache), P(c_cache), vp, vp, vp, vp, vp]
     lib.kvr_fork.restype = ctypes.c_int
     lib.kvr_append.argtypes = [P(c_cache), vp, i32, vp, vp, vp, vp]
@@ -272,3 +283,39 @@ def append(cache: Cache, len_: torch.Tensor, k_new: torch.Tensor, v_new: torch.T
     rc = lib.kvr_append(ctypes.byref(cc), _ptr(len_), k_new.shape[3], _ptr(k_new), _ptr(v_new),
                         _ptr(pos_new), _stream(stream))
     _check(rc, "kvr_append")
+
+
+@dataclass
+class Sampler:
+    """Sampling settings of kvr_logit_entropy_sample (decoding setup of the paper:
+    temperature 0.8, top-k 20, top-p 0.95)."""
+    temperature: float = 0.8
+    top_k: int = 20
+    top_p: float = 0.95
+    seed: int = 0
+    step: int = 0
+
+    def c(self) -> c_sampler:
+        return c_sampler(self.temperature, self.top_k, self.top_p, self.seed, self.step)
+
+
+def logit_entropy_sample_workspace_size(R: int, V: int, top_k: int) -> int:
+    return int(lib.kvr_logit_entropy_sample_workspace_size(R, V, top_k))
+
+
+def logit_entropy_sample(logits: torch.Tensor, H: torch.Tensor, tokens: torch.Tensor,
+                         sampler: Sampler, V: Optional[int] = None, inv_temp: float = 1.0,
+                         detector: Optional[Detector] = None,
+                         workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """kvr_logit_entropy_sample: entropy (and detector) plus one sampled token per row."""
+    assert logits.dim() == 2 and logits.stride(1) == 1
+    R, ld = logits.shape[0], logits.stride(0)
+    V = logits.shape[1] if V is None else V
+    det = detector.c() if detector is not None else None
+    smp = sampler.c()
+    rc = lib.kvr_logit_entropy_sample(_ptr(logits), dtype_code(logits.dtype), R, V, ld,
+                                      float(inv_temp), _ptr(H), ctypes.byref(det) if det else None,
+                                      ctypes.byref(smp), _ptr(tokens), _ptr(workspace),
+                                      0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                      _stream(stream))
+    _check(rc, "kvr_logit_entropy_sample")

@@ -13,9 +13,11 @@ The second form turns one FETCH_SIZE pass and one WRITE_SIZE pass into HBM
 bytes per library call: each counter is scaled by the factor that maps its
 reading on a plain copy kernel of known size (N bytes read and N bytes
 written per dispatch; the copy whose WRITE_SIZE is within 10% of N) onto N,
-and the kernels that make up one call (CALL_KERNELS) are summed. The record
-carries a hash of the kernel sources so that a reader can tell whether it
-was taken on the kernels it runs.
+and the kernels that make up one call (CALL_KERNELS) are summed. Each call's
+entry carries a hash of its kernel sources (CALL_SOURCES) so that a reader
+can tell whether it was taken on the kernels it runs. Per-dispatch averages
+run over every dispatch of the profiled program, so the passes should run
+the same steps as the measurement they are compared with.
 """
 from __future__ import annotations
 
@@ -29,7 +31,13 @@ import re
 import sqlite3
 
 CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
-KERNEL_SOURCES = ("attn.hip", "evict.hip", "entropy.hip", "kvr_device.h")
+# Sources whose kernels each call runs (a record stays valid while they do not change).
+CALL_SOURCES = {
+    "base_attn": ("attn.hip", "kvr_device.h"),
+    "helper_attn": ("attn.hip", "kvr_device.h"),
+    "evict": ("evict.hip", "kvr_device.h"),
+    "entropy": ("entropy.hip", "kvr_device.h"),
+}
 
 # Kernels launched by one call of each hot-path entry point, by call name.
 CALL_KERNELS = {
@@ -40,9 +48,10 @@ CALL_KERNELS = {
 }
 
 
-def kernel_source_hash() -> str:
+def source_hash(call: str) -> str:
+    """Hash of the kernel sources behind one call (see CALL_SOURCES)."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in CALL_SOURCES[call]:
         with open(os.path.join(CSRC, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -124,8 +133,8 @@ def traffic(fetch_dir: str, write_dir: str, calib_bytes: int, workload: str) -> 
             wr += parts[-1]["write_bytes"]
         else:
             calls[call] = dict(read_bytes=int(rd), write_bytes=int(wr), bytes_per_call=int(rd + wr),
-                               kernels=parts)
-    return dict(workload=workload, kernel_source_hash=kernel_source_hash(),
+                               source_hash=source_hash(call), kernels=parts)
+    return dict(workload=workload,
                 calibration=dict(kernel=tag, bytes=calib_bytes, fetch_factor=round(f_read, 4),
                                  write_factor=round(f_write, 4)),
                 calls=calls)

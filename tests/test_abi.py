@@ -116,3 +116,22 @@ def test_append_rejects_bad_arguments_on_host():
     assert kvr.lib.kvr_append(ctypes.byref(c), 16, 1 << 30, 16, 16, None, None) == -2
     # T == 0 enqueues nothing and needs no token arrays
     assert kvr.lib.kvr_append(ctypes.byref(c), 16, 0, None, None, None, None) == 0
+
+
+def test_sampler_rejects_bad_arguments_on_host():
+    from paper_2608_15797_amd import kvr
+    f = kvr.lib.kvr_logit_entropy_sample
+    need = kvr.lib.kvr_logit_entropy_sample_workspace_size(8, 151936, 20)
+    assert need > 0 and need % 16 == 0
+    assert kvr.lib.kvr_logit_entropy_sample_workspace_size(8, 151936, 65) == 0
+    good = kvr.c_sampler(0.8, 20, 0.95, 1, 2)
+    for smp, msg in ((kvr.c_sampler(0.0, 20, 0.95, 0, 0), "temperature"),
+                     (kvr.c_sampler(0.8, 0, 0.95, 0, 0), "top_k"),
+                     (kvr.c_sampler(0.8, 65, 0.95, 0, 0), "top_k"),
+                     (kvr.c_sampler(0.8, 20, 0.0, 0, 0), "top_p"),
+                     (kvr.c_sampler(0.8, 20, 1.01, 0, 0), "top_p")):
+        rc = f(16, 1, 8, 1024, 1024, 1.0, 16, None, ctypes.byref(smp), 16, 16, 1 << 20, None)
+        assert rc == -1 and msg in kvr.lib.kvr_last_error().decode()
+    # tokens are required; a workspace is always required
+    assert f(16, 1, 8, 1024, 1024, 1.0, 16, None, ctypes.byref(good), None, 16, 1 << 20, None) == -1
+    assert f(16, 1, 8, 1024, 1024, 1.0, 16, None, ctypes.byref(good), 16, None, 0, None) == -4
