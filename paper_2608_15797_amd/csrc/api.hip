@@ -79,8 +79,10 @@ const char *kvr_last_error(void) { return g_err; }
 
 size_t kvr_decode_attn_workspace_size(const kvr_cache *cache, const kvr_prefix *prefix, int32_t Hq) {
   if (!cache || !prefix || prefix->P <= 0 || cache->dtype != KVR_BF16) return 0;
-  int ns = 1, ch = 64;
-  kvr::plan_prefix_splits(prefix->P, cache->L, cache->Hkv, prefix->plen, &ns, &ch);
+  if (cache->Hkv <= 0 || Hq <= 0 || Hq % cache->Hkv != 0 || cache->S % prefix->P != 0) return 0;
+  int ns = 1, span = 1, nw = 1;
+  const int rows = (cache->S / prefix->P) * (Hq / cache->Hkv);
+  kvr::plan_prefix_splits(cache->D, prefix->P, cache->L, cache->Hkv, prefix->plen, rows, &ns, &span, &nw);
   return kvr::attn_workspace_bytes(cache->S, cache->L, Hq, cache->D, ns);
 }
 
@@ -129,7 +131,7 @@ int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int3
     if (cache->dtype == KVR_BF16) {
       if (p.C * G > 64)
         return fail(KVR_EUNSUPPORTED, "%d candidates x %d heads per shared prefix exceeds 64 rows", p.C, G);
-      kvr::plan_prefix_splits(p.P, p.L, p.Hkv, p.plen, &p.nsplit, &p.chunk);
+      kvr::plan_prefix_splits(p.D, p.P, p.L, p.Hkv, p.plen, p.C * G, &p.nsplit, &p.span, &p.nwaves);
       const size_t need = kvr::attn_workspace_bytes(p.S, p.L, Hq, p.D, p.nsplit);
       if (!workspace || workspace_bytes < need)
         return fail(KVR_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);

@@ -24,15 +24,19 @@
 // domain. Logits of window steps go to LDS so the normalised probabilities
 // can be summed over the G heads after the last chunk.
 //
-// Helper (prefix) path: split-K over the prefix; one wave per
-// (prefix, layer, KV head, split) processes the query rows of all candidates
-// sharing the prefix (up to 4 row blocks = 64 rows), so shared context is
-// read from HBM once per step, and writes (max, sum, unnormalised o)
-// partials. The private suffix then runs as its own unit per (candidate,
-// layer, KV head) and folds those partials in by log-sum-exp.
+// Helper (prefix) path: split-K over the prefix. Each wave processes the query
+// rows of all candidates sharing a prefix (up to 4 row blocks = 64 rows), so
+// shared context is read from HBM once per step, and writes (max, sum,
+// unnormalised o) partials. The waves are exactly as many as fit on the chip
+// at once, each taking an equal span of the flattened (prefix, layer, KV
+// head, key) space (one partial per unit its span touches), so all of them
+// finish in one round. The private suffix then runs as its own unit per
+// (candidate, layer, KV head) and folds those partials in by log-sum-exp.
 //
 // f32 path: plain VALU kernel (one wave per unit) for float32 caches.
 #include <hip/hip_runtime.h>
+
+#include <atomic>
 
 #include "kvr_device.h"
 #include "kvr_internal.h"
@@ -395,13 +399,16 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
       if (row < G) {
         const size_t stride = (size_t)p.S * p.L * p.Hq * (D + 4);
         const float *r0 = p.ws + ((((size_t)s * p.L + l) * p.Hq + qh0 + row) * (D + 4));
+        // Pieces of this row's context unit: the waves whose spans touch it.
+        const long ug = ((long)((s / p.C) * p.L + l) * p.Hkv + h) * p.plen;
+        const int npieces = (int)((ug + p.plen - 1) / p.span - ug / p.span) + 1;
         float M = mi;
-        for (int k = 0; k < p.nsplit; k++) M = fmaxf(M, r0[k * stride]);
+        for (int k = 0; k < npieces; k++) M = fmaxf(M, r0[k * stride]);
         const float wown = fast_exp2(mi - M);
         zi *= wown;
 #pragma unroll
         for (int b = 0; b < NB; b++) o[b][i] *= wown;
-        for (int k = 0; k < p.nsplit; k++) {
+        for (int k = 0; k < npieces; k++) {
           const float *r = r0 + k * stride;
           const float mk = r[0];
           const float w = mk == kNegInf ? 0.0f : fast_exp2(mk - M);
@@ -451,32 +458,41 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Prefix kernel: one wave per (prefix, layer, KV head, split); RB row blocks
-// of 16 rows hold the C*G query rows (candidate c, head g) sharing the prefix,
-// so each prefix byte is read once per step for all of them. Same
-// double-buffered chunk stream as the own-cache kernel.
+// Prefix kernel: each wave walks its span of the flattened (prefix, layer,
+// KV head, key) space one unit segment at a time; RB row blocks of 16 rows
+// hold the C*G query rows (candidate c, head g) sharing the prefix, so each
+// prefix byte is read once per step for all of them. Same double-buffered
+// chunk stream as the own-cache kernel.
 template <int D, int RB, int TILES, int DEPTH>
 __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
   constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
   constexpr uint32_t ROW = D * 2;
-  const int nunits = p.P * p.L * p.Hkv;
-  const int split = blockIdx.x / nunits;
-  const int unit = blockIdx.x % nunits;  // ((pp * L) + l) * Hkv + h
-  const int h = unit % p.Hkv;
-  const int pl = unit / p.Hkv;
-  const int l = pl % p.L;
-  const int pp = pl / p.L;
+  const long total = (long)p.P * p.L * p.Hkv * p.plen;
+  const long g0 = (long)blockIdx.x * p.span;
+  const long g1 = g0 + p.span < total ? g0 + p.span : total;
   const int lane = threadIdx.x;
   const int r16 = lane & 15;
   const int g4 = lane >> 4;
   const int G = p.G;
   const int rows = p.C * G;
 
+  // This wave's keys [g0, g1) of the flattened (unit, key) space, one segment
+  // per unit it touches; each segment leaves one partial record per row.
+#pragma clang loop unroll(disable)
+  for (long g = g0; g < g1;) {
+  const int unit = (int)(g / p.plen);  // ((pp * L) + l) * Hkv + h
+  const int k0 = (int)(g - (long)unit * p.plen);
+  const int k1 = (int)((long)p.plen < k0 + (g1 - g) ? (long)p.plen : k0 + (g1 - g));
+  const int split = blockIdx.x - (int)((long)unit * p.plen / p.span);  // piece index within the unit
+  g += k1 - k0;
+  const int h = unit % p.Hkv;
+  const int pl = unit / p.Hkv;
+  const int l = pl % p.L;
+  const int pp = pl / p.L;
+
   const bf16_t *Kp = static_cast<const bf16_t *>(p.pk) + (size_t)unit * p.plen * D;
   const bf16_t *Vp = static_cast<const bf16_t *>(p.pv) + (size_t)unit * p.plen * D;
-  const int k0 = split * p.chunk;
-  const int k1 = min(k0 + p.chunk, p.plen);
 
   short4_t qop[RB][NB];
 #pragma unroll
@@ -549,6 +565,7 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
       }
     }
   }
+  }  // segments
 }
 
 // ---------------------------------------------------------------------------
@@ -653,11 +670,11 @@ hipError_t launch_bf16(const AttnParams &p, hipStream_t stream) {
   }
   // Context splits first; the suffix kernel then merges their partials.
   const int rb = (p.C * p.G + 15) / 16;
-  const dim3 gridA(p.P * p.L * p.Hkv * p.nsplit);
+  const dim3 gridA(p.nwaves);
   switch (rb) {
     case 1: hipLaunchKernelGGL((attn_prefix_bf16<D, 1, 2, 2>), gridA, dim3(64), 0, stream, p); break;
     case 2: hipLaunchKernelGGL((attn_prefix_bf16<D, 2, 2, 2>), gridA, dim3(64), 0, stream, p); break;
-    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3, 2, 2>), gridA, dim3(64), 0, stream, p); break;
+    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3, 1, 2>), gridA, dim3(64), 0, stream, p); break;
     case 4: hipLaunchKernelGGL((attn_prefix_bf16<D, 4, 1, 2>), gridA, dim3(64), 0, stream, p); break;
     default: return hipErrorInvalidValue;
   }
@@ -673,19 +690,55 @@ size_t f32_attn_lds_bytes(int G, int D, int plen, int cap) {
   return ((size_t)G * D + (size_t)G * (plen + cap) + 32) * sizeof(float);
 }
 
-void plan_prefix_splits(int P, int L, int Hkv, int plen, int *nsplit, int *chunk) {
-  // Aim for >= 2048 waves over the prefix, with chunks of at least 512 keys
-  // (multiples of 64 so every chunk but the last is whole tiles).
-  const long units = (long)P * L * Hkv;
-  long ns = (2048 + units - 1) / units;
-  const long maxs = (plen + 511) / 512;
-  if (ns > maxs) ns = maxs;
-  if (ns < 1) ns = 1;
-  long ch = (plen + ns - 1) / ns;
-  ch = (ch + 63) / 64 * 64;
-  ns = (plen + ch - 1) / ch;
-  *nsplit = (int)(ns < 1 ? 1 : ns);
-  *chunk = (int)(ch < 64 ? 64 : ch);
+namespace {
+
+// Waves of one prefix-kernel instantiation that fit on the device at once
+// (occupancy per CU x CU count), looked up once per instantiation.
+template <int D, int RB, int TILES>
+int prefix_slots() {
+  static std::atomic<int> cached{0};
+  int v = cached.load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_prefix_bf16<D, RB, TILES, 2>, 64, 0) !=
+          hipSuccess || per_cu <= 0)
+    per_cu = 4;
+  v = cus * per_cu;
+  cached.store(v, std::memory_order_relaxed);
+  return v;
+}
+
+template <int D>
+int prefix_slots_for(int rb) {
+  switch (rb) {
+    case 1: return prefix_slots<D, 1, 2>();
+    case 2: return prefix_slots<D, 2, 2>();
+    case 3: return prefix_slots<D, 3, 1>();
+    default: return prefix_slots<D, 4, 1>();
+  }
+}
+
+}  // namespace
+
+void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int *nsplit, int *span,
+                        int *nwaves) {
+  // One round of waves: as many as fit on the chip at once, each taking an
+  // equal span (whole 32-key chunks, at least 512 keys) of the flattened
+  // (prefix, layer, KV head, key) space. A unit of plen keys is then covered
+  // by at most ceil(plen / span) + 1 spans.
+  const int rb = (rows + 15) / 16;
+  const long total = (long)P * L * Hkv * plen;
+  const long slots = D == 128 ? prefix_slots_for<128>(rb) : prefix_slots_for<64>(rb);
+  long sp = (total + slots - 1) / slots;
+  sp = (sp + 31) / 32 * 32;
+  if (sp < 512) sp = 512;
+  const long nw = (total + sp - 1) / sp;
+  *span = (int)sp;
+  *nwaves = (int)nw;
+  *nsplit = (int)((plen + sp - 1) / sp + 1);
 }
 
 size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit) {

@@ -26,13 +26,18 @@ struct AttnParams {
   // scoring (scores == nullptr: off)
   float *scores;
   int B, W, buffer;
-  // split-K partials for the prefix path: ws [nsplit][S][L][Hq][D+4] floats
+  // split-K partials for the prefix path: ws [nsplit][S][L][Hq][D+4] floats.
+  // The context kernel's nwaves waves each take `span` consecutive keys of
+  // the flattened (prefix, layer, KV head, key) space; a unit is covered by at
+  // most nsplit of them, each leaving one partial record.
   float *ws;
-  int nsplit, chunk;
+  int nsplit, span, nwaves;
 };
 
-// Split plan for the prefix path; identical on the size query and the call.
-void plan_prefix_splits(int P, int L, int Hkv, int plen, int *nsplit, int *chunk);
+// Work plan of the prefix path (rows = C * G query rows per prefix unit);
+// identical on the size query and the call.
+void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int *nsplit, int *span,
+                        int *nwaves);
 size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit);
 
 hipError_t launch_decode_attn(const AttnParams &p, hipStream_t stream);
