@@ -135,3 +135,21 @@ def test_sampler_rejects_bad_arguments_on_host():
     # tokens are required; a workspace is always required
     assert f(16, 1, 8, 1024, 1024, 1.0, 16, None, ctypes.byref(good), None, 16, 1 << 20, None) == -1
     assert f(16, 1, 8, 1024, 1024, 1.0, 16, None, ctypes.byref(good), 16, None, 0, None) == -4
+
+
+def test_lds_limits_rejected_on_host():
+    """One step past each kernel's LDS bound is refused before any launch."""
+    from paper_2608_15797_amd import kvr
+    # Scored decode at G = 16: cap 961 rounds to 1024 slots of logits per head.
+    c = _cache(kvr, Hkv=1, cap=961)
+    pol = kvr.c_policy(704, 64, 256)
+    rc = kvr.lib.kvr_decode_attn(ctypes.byref(c), None, 16, 16, 16, 1.0, None, None, None, 16,
+                                 ctypes.byref(pol), 16, None, 0, None)
+    assert rc == -2 and "LDS" in kvr.lib.kvr_last_error().decode()
+    # Eviction: (2 cap + B) words of LDS.
+    c = _cache(kvr, cap=8100)
+    pol = kvr.c_policy(256, 32, 7843)
+    assert kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, 16, ctypes.byref(pol), None, None) == -2
+    # Window recompute (bf16): cap words of LDS.
+    c = _cache(kvr, cap=16385)
+    assert kvr.lib.kvr_accumulate_scores(ctypes.byref(c), 16, 16, 8, 8, 1.0, 16, 0, None) == -2

@@ -50,6 +50,8 @@ BASE_CASES = [
     (3, 2, 2, 6, 64, 40, 8, 30, torch.bfloat16),
     (2, 1, 1, 16, 128, 20, 5, 7, torch.bfloat16),
     (2, 2, 3, 1, 128, 20, 5, 7, torch.bfloat16),
+    # Largest scored cache at G = 16: the window logits fill 61.6 KB of LDS (limit 64 KB).
+    (2, 1, 1, 16, 128, 704, 64, 255, torch.bfloat16),
 ]
 
 
@@ -235,6 +237,8 @@ EVICT_CASES = [
     (4, 3, 4, 128, 128, 32, 128, torch.bfloat16),
     (6, 2, 8, 128, 64, 32, 64, torch.bfloat16),
     (3, 2, 2, 128, 20, 5, 7, torch.float32),
+    # Largest cache the eviction kernel takes at B = 256: cap 8000, 63.5 KB of LDS.
+    (1, 1, 2, 128, 256, 32, 7743, torch.bfloat16),
 ]
 
 
@@ -339,6 +343,7 @@ def test_evict_topb_ties_and_gpu_scores_selection():
     (torch.bfloat16, 128, 16, 33, 130),    # 33 row blocks: the last pair is half empty
     (torch.bfloat16, 128, 1, 3, 40),       # fewer rows than one block
     (torch.bfloat16, 128, 7, 128, 300),    # a committed step's window on the 7B head shape
+    (torch.bfloat16, 128, 4, 8, 16384),    # largest cache: the accumulator fills 64 KB of LDS
 ])
 def test_accumulate_scores(dt, D, G, nq, cap):
     """kvr_accumulate_scores equals the oracle's causal window re-computation,
