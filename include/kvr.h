@@ -211,6 +211,30 @@ int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scor
                    const kvr_policy *policy, int32_t *kept, hipStream_t stream);
 
 /*
+ * kvr_redundancy_scores -- redundancy-aware eviction score: query-attention
+ * importance mixed with key redundancy (cosine similarity) with weight lambda,
+ * after pooling (App. C, KV eviction; App. D.3). The paper names these parts
+ * but gives no formula; this is the reading implemented. For every sequence
+ * with n = len[s] > B + buffer and every (layer, KV head), over the candidates
+ * c < m = n - W:
+ *   P_c   = max of importance over the candidates within pool/2 slots of c;
+ *   R_c   = mean cosine similarity of key c to the other m - 1 candidate keys
+ *           (a zero key has cosine 0 with every key);
+ *   out_c = lam * P_c / sum_c' P_c' - (1 - lam) * softmax_c(R)
+ *           (the importance term is 1/m when all P are 0).
+ * Other slots and sequences are not written. Feed `out` to kvr_evict_topb.
+ *
+ *   importance : [S][L][Hkv][cap] float32, e.g. the window scores streamed by
+ *                kvr_decode_attn; `out` may be the same array.
+ *   lam        : in [0, 1]; the paper uses 0.1.  pool : >= 1 (7 is common).
+ * Errors: KVR_EINVAL (pointer, policy, lambda, pool), KVR_EUNSUPPORTED (dtype,
+ * D, LDS: 3 cap + 5 D + 4 floats must fit in 64 KiB), KVR_EHIP.
+ */
+int kvr_redundancy_scores(const kvr_cache *cache, const int32_t *len, const float *importance,
+                          const kvr_policy *policy, float lam, int32_t pool, float *out,
+                          hipStream_t stream);
+
+/*
  * kvr_logit_entropy -- token entropy H = -sum_v p(v) log p(v) of
  * p = softmax(inv_temp * logits) for R rows (Eq. (4)), natural log.
  *

@@ -24,7 +24,9 @@ Everything is timed with the library's own kernels on the 7B shape (28 layers,
     streamed during the last W steps; one TopB eviction at the end);
   * evicted, per step: the cost model in which scoring and eviction run every
     step once l > B' (the setting the paper's alpha refers to): one scored
-    attention step at B'+1 plus one TopB eviction.
+    attention step at B'+1 plus one TopB eviction; and the same with the
+    redundancy-aware score (pooled importance mixed with key cosine
+    similarity) computed before each eviction.
 A least-squares line t(l) = a + b l is fitted to the full-KV times, then
   alpha = t_evict / t(B') - 1   and   l* = (t_evict - a) / b,
 which is (1 + alpha) B' when the intercept a is small.
@@ -94,9 +96,11 @@ def evicted_ms(S, L, Hq, Hkv, D, B, W, buffer, reps=3, seed=7):
     t_scored = _time(lambda: step(len(lens) - 1), 50)
     t_evict = _time(lambda: kvr.evict_topb(cache, last, scores, pol), 50)
     t_plain = _time(lambda: step(len(lens) - 2, scored=False), 50)
-    del cache, scores
+    mixed = torch.empty_like(scores)
+    t_red = _time(lambda: kvr.redundancy_scores(cache, last, scores, pol, mixed), 50)
+    del cache, scores, mixed
     torch.cuda.empty_cache()
-    return t_cycle, t_scored, t_evict, t_plain
+    return t_cycle, t_scored, t_evict, t_plain, t_red
 
 
 def full_ms(S, L, Hq, Hkv, D, ell, reps=10, seed=11):
@@ -144,7 +148,7 @@ def fit_line(xs, ys):
 def measure(S=16, B=512, W=128, buffer=128,
             lengths=(640, 1024, 2048, 3072, 4096, 6144, 8192, 12288, 16384)):
     L, Hq, Hkv, D = QWEN7B["L"], QWEN7B["Hq"], QWEN7B["Hkv"], QWEN7B["D"]
-    t_cycle, t_scored, t_evict, t_plain = evicted_ms(S, L, Hq, Hkv, D, B, W, buffer)
+    t_cycle, t_scored, t_evict, t_plain, t_red = evicted_ms(S, L, Hq, Hkv, D, B, W, buffer)
     full = {}
     for ell in lengths:
         full[ell] = full_ms(S, L, Hq, Hkv, D, ell)
@@ -155,6 +159,7 @@ def measure(S=16, B=512, W=128, buffer=128,
     Bp = B + buffer
     t_bp = a + b * Bp
     t_step = t_scored + t_evict
+    t_rkv = t_scored + t_red + t_evict
 
     def cross(t):
         return dict(ms=round(t, 5), alpha=round(t / t_bp - 1.0, 3),
@@ -166,8 +171,9 @@ def measure(S=16, B=512, W=128, buffer=128,
                          for k, v in full.items()},
                 fit=dict(intercept_ms=round(a, 5), ms_per_token=b, at_B_prime_ms=round(t_bp, 5)),
                 parts_ms=dict(scored_step=round(t_scored, 5), eviction=round(t_evict, 5),
-                              unscored_step=round(t_plain, 5)),
-                evicted_amortised=cross(t_cycle), evicted_every_step=cross(t_step))
+                              unscored_step=round(t_plain, 5), redundancy=round(t_red, 5)),
+                evicted_amortised=cross(t_cycle), evicted_every_step=cross(t_step),
+                evicted_every_step_redundancy=cross(t_rkv))
 
 
 def main(argv=None):

@@ -189,6 +189,27 @@ int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scor
   return hip_status(kvr::launch_evict_topb(p, stream), "kvr_evict_topb launch");
 }
 
+int kvr_redundancy_scores(const kvr_cache *cache, const int32_t *len, const float *importance,
+                          const kvr_policy *policy, float lam, int32_t pool, float *out,
+                          hipStream_t stream) {
+  int G = 0;
+  int st = check_cache(cache, 0, &G);
+  if (st) return st;
+  if (!len || !importance || !out || !policy)
+    return fail(KVR_EINVAL, "len, importance, policy and out are required");
+  st = check_policy(policy, cache->cap);
+  if (st) return st;
+  if (!(lam >= 0.f && lam <= 1.f)) return fail(KVR_EINVAL, "lambda must lie in [0, 1]");
+  if (pool < 1) return fail(KVR_EINVAL, "pool=%d must be at least 1", pool);
+  const size_t lds = kvr::redundancy_lds_bytes(cache->cap, cache->D);
+  if (lds > 65536) return fail(KVR_EUNSUPPORTED, "cap=%d needs %zu bytes of LDS (> 64 KiB)", cache->cap, lds);
+  kvr::RedundancyParams p{};
+  p.k = cache->k; p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.cap = cache->cap;
+  p.D = cache->D; p.dtype = cache->dtype; p.len = len; p.importance = importance; p.out = out;
+  p.B = policy->B; p.W = policy->W; p.buffer = policy->buffer; p.pool = pool; p.lam = lam;
+  return hip_status(kvr::launch_redundancy(p, stream), "kvr_redundancy_scores launch");
+}
+
 int kvr_fork(const kvr_cache *src, const kvr_cache *dst, const int32_t *src_index,
              const int32_t *len, const float *src_scores, float *dst_scores,
              hipStream_t stream) {

@@ -65,6 +65,18 @@ struct EvictParams {
 };
 hipError_t launch_evict_topb(const EvictParams &p, hipStream_t stream);
 
+struct RedundancyParams {
+  const void *k;
+  int S, L, Hkv, cap, D, dtype;
+  const int32_t *len;
+  const float *importance;
+  float *out;
+  int B, W, buffer, pool;
+  float lam;
+};
+size_t redundancy_lds_bytes(int cap, int D);
+hipError_t launch_redundancy(const RedundancyParams &p, hipStream_t stream);
+
 struct EntropyParams {
   const void *logits;
   int dtype;

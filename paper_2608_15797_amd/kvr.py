@@ -25,7 +25,8 @@ STATUS = {0: "KVR_OK", -1: "KVR_EINVAL", -2: "KVR_EUNSUPPORTED", -3: "KVR_EHIP",
 EXPORTS = ("kvr_strerror", "kvr_last_error", "kvr_decode_attn", "kvr_decode_attn_workspace_size",
            "kvr_accumulate_scores", "kvr_evict_topb", "kvr_logit_entropy",
            "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append",
-           "kvr_logit_entropy_sample", "kvr_logit_entropy_sample_workspace_size")
+           "kvr_logit_entropy_sample", "kvr_logit_entropy_sample_workspace_size",
+           "kvr_redundancy_scores")
 
 
 class KvrError(RuntimeError):
@@ -89,6 +90,8 @@ def _load():
     lib.kvr_logit_entropy_sample.restype = ctypes.c_int
     lib.kvr_logit_entropy_sample_workspace_size.argtypes = [i32, i32, i32]
     lib.kvr_logit_entropy_sample_workspace_size.restype = sz
+    lib.kvr_redundancy_scores.argtypes = [P(c_cache), vp, vp, P(c_policy), f32, i32, vp, vp]
+    lib.kvr_redundancy_scores.restype = ctypes.c_int
     lib.kvr_fork.argtypes = [P(c_cache), P(c_cache), vp, vp, vp, vp, vp]
     lib.kvr_fork.restype = ctypes.c_int
     lib.kvr_append.argtypes = [P(c_cache), vp, i32, vp, vp, vp, vp]
@@ -319,3 +322,15 @@ def logit_entropy_sample(logits: torch.Tensor, H: torch.Tensor, tokens: torch.Te
                                       0 if workspace is None else workspace.numel() * workspace.element_size(),
                                       _stream(stream))
     _check(rc, "kvr_logit_entropy_sample")
+
+
+def redundancy_scores(cache: Cache, len_: torch.Tensor, importance: torch.Tensor, policy: Policy,
+                      out: torch.Tensor, lam: float = 0.1, pool: int = 7, stream=None) -> None:
+    """kvr_redundancy_scores: pooled importance mixed with mean key cosine
+    similarity, for sequences that evict this step; feed `out` to evict_topb."""
+    cc = cache.c()
+    pol = policy.c()
+    assert importance.is_contiguous() and out.is_contiguous()
+    rc = lib.kvr_redundancy_scores(ctypes.byref(cc), _ptr(len_), _ptr(importance), ctypes.byref(pol),
+                                   float(lam), int(pool), _ptr(out), _stream(stream))
+    _check(rc, "kvr_redundancy_scores")
