@@ -82,6 +82,10 @@ __device__ __forceinline__ void load_qop(const bf16_t *qrow, int g4, short4_t (&
 // Buffer resources: a wave-uniform base address and byte range in SGPRs, so
 // per-lane addressing is a 32-bit offset and loads past the range return 0.
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// s_waitcnt vmcnt(0), other counters unconstrained.
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
@@ -323,6 +327,27 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   const int ncache = append ? n - 1 : n;
 
   const int qh0 = h * G;
+  // Merge: the partial records of this wave's rows, piece k at stride
+  // S*L*Hq*(D+4) floats, G contiguous records each. The first merge_pf pieces
+  // are copied into LDS now (buffer-to-LDS loads, 1 KiB per instruction) so
+  // the epilogue does not wait on them.
+  int npieces = 0, pf = 0;
+  const size_t rstride = (size_t)p.S * p.L * p.Hq * (D + 4);
+  const float *rbase = nullptr;
+  if constexpr (MERGE) {
+    const long ug = ((long)((s / p.C) * p.L + l) * p.Hkv + h) * p.plen;
+    npieces = (int)((ug + p.plen - 1) / p.span - ug / p.span) + 1;
+    pf = npieces < p.merge_pf ? npieces : p.merge_pf;
+    rbase = p.ws + (((size_t)s * p.L + l) * p.Hq + qh0) * (D + 4);
+#if defined(__HIP_DEVICE_COMPILE__)
+    for (int k = 0; k < pf; k++) {
+      const rsrc_t rr = make_rsrc(rbase + k * rstride, (uint32_t)G * (D + 4) * 4u);
+      for (int j = 0; j < p.merge_blk / 256; j++)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void_t *)(smem + k * p.merge_blk + j * 256), 16,
+                                                 (uint32_t)(j * 1024 + lane * 16), 0, 0, 0);
+    }
+#endif
+  }
   const size_t qrow0 = ((size_t)s * p.L + l) * p.Hq + qh0;
   short4_t qop[NB];
   load_qop<D>(r16 < G ? static_cast<const bf16_t *>(p.q) + (qrow0 + r16) * D : nullptr, g4, qop);
@@ -396,20 +421,20 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
       // Log-sum-exp merge with the context partials of this row:
       // record = (max, sum, -, -, unnormalised o[D]) in the log2 domain.
       const float mi = __shfl(st.m, row, kWave);
+      if (i == 0) wait_vm0();  // the LDS copies of the partials have landed
       if (row < G) {
-        const size_t stride = (size_t)p.S * p.L * p.Hq * (D + 4);
-        const float *r0 = p.ws + ((((size_t)s * p.L + l) * p.Hq + qh0 + row) * (D + 4));
-        // Pieces of this row's context unit: the waves whose spans touch it.
-        const long ug = ((long)((s / p.C) * p.L + l) * p.Hkv + h) * p.plen;
-        const int npieces = (int)((ug + p.plen - 1) / p.span - ug / p.span) + 1;
+        // Piece k of this row's record: in LDS for k < pf, else in the workspace.
+        auto rec = [&](int k) -> const float * {
+          return k < pf ? smem + k * p.merge_blk + row * (D + 4) : rbase + k * rstride + row * (D + 4);
+        };
         float M = mi;
-        for (int k = 0; k < npieces; k++) M = fmaxf(M, r0[k * stride]);
+        for (int k = 0; k < npieces; k++) M = fmaxf(M, rec(k)[0]);
         const float wown = fast_exp2(mi - M);
         zi *= wown;
 #pragma unroll
         for (int b = 0; b < NB; b++) o[b][i] *= wown;
         for (int k = 0; k < npieces; k++) {
-          const float *r = r0 + k * stride;
+          const float *r = rec(k);
           const float mk = r[0];
           const float w = mk == kNegInf ? 0.0f : fast_exp2(mk - M);
           zi += r[1] * w;
@@ -661,7 +686,15 @@ __global__ __launch_bounds__(64) void attn_f32(AttnParams p, int nt_max) {
 }
 
 template <int D>
-hipError_t launch_bf16(const AttnParams &p, hipStream_t stream) {
+hipError_t launch_bf16(const AttnParams &p_in, hipStream_t stream) {
+  AttnParams p = p_in;
+  if (p.P > 0) {
+    // LDS for the suffix kernel's prefetched partials: whole 1 KiB blocks per
+    // piece, at most 16 KiB per wave (8 waves per CU then use 128 of 160 KiB).
+    p.merge_blk = (p.G * (D + 4) * 4 + 1023) / 1024 * 256;
+    const int fit = 16384 / (p.merge_blk * 4);
+    p.merge_pf = p.nsplit < fit ? p.nsplit : fit;
+  }
   const dim3 units(p.S * p.L * p.Hkv);
   if (p.P == 0) {
     const size_t lds = p.scores ? ((size_t)p.G * ((p.cap + 63) & ~63) + 32) * sizeof(float) : 0;
@@ -680,7 +713,8 @@ hipError_t launch_bf16(const AttnParams &p, hipStream_t stream) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_cache_bf16<D, true, 2, 2>), units, dim3(64), 0, stream, p);
+  hipLaunchKernelGGL((attn_cache_bf16<D, true, 2, 2>), units, dim3(64),
+                     (size_t)p.merge_pf * p.merge_blk * sizeof(float), stream, p);
   return hipGetLastError();
 }
 

@@ -32,6 +32,9 @@ struct AttnParams {
   // most nsplit of them, each leaving one partial record.
   float *ws;
   int nsplit, span, nwaves;
+  // The suffix kernel prefetches the first merge_pf pieces of its rows'
+  // partials into LDS (merge_blk floats per piece) at wave start.
+  int merge_pf, merge_blk;
 };
 
 // Work plan of the prefix path (rows = C * G query rows per prefix unit);
