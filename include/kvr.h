@@ -246,6 +246,7 @@ int kvr_redundancy_scores(const kvr_cache *cache, const int32_t *len, const floa
  *   workspace : at least kvr_logit_entropy_workspace_size(R, V) bytes of
  *            device scratch for per-split partial sums (no initialisation
  *            needed). May be NULL/0 when that size is 0.
+ *   inv_temp : positive and finite (KVR_EINVAL otherwise).
  * -inf logits are allowed (they contribute 0); a row of only -inf is invalid.
  */
 int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, int64_t ld,

@@ -3,6 +3,8 @@
 // anything; on error it returns a status and records a message retrievable
 // with kvr_last_error() on the same thread.
 #include <hip/hip_runtime.h>
+
+#include <cmath>
 #include <stdarg.h>
 #include <stdio.h>
 
@@ -29,8 +31,7 @@ int hip_status(hipError_t e, const char *what) {
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Shared checks of a cache description; sets G when Hq > 0.
-int check_cache(const kvr_cache *c, int32_t Hq, int *G, bool need_pos_ok = true) {
-  (void)need_pos_ok;
+int check_cache(const kvr_cache *c, int32_t Hq, int *G) {
   if (!c) return fail(KVR_EINVAL, "cache is NULL");
   if (!c->k || !c->v) return fail(KVR_EINVAL, "cache k/v pointer is NULL");
   if (c->S <= 0 || c->L <= 0 || c->Hkv <= 0 || c->cap <= 0 || c->D <= 0)
@@ -276,6 +277,8 @@ int entropy_params(const void *logits, int32_t dtype, int32_t R, int32_t V, int6
   if (dtype != KVR_F32 && dtype != KVR_BF16) return fail(KVR_EUNSUPPORTED, "dtype %d", dtype);
   if (R <= 0 || V <= 0 || ld < V) return fail(KVR_EINVAL, "need R > 0, V > 0, ld >= V (R=%d V=%d ld=%ld)", R, V, (long)ld);
   if (R > 65535) return fail(KVR_EUNSUPPORTED, "R=%d rows exceeds 65535", R);
+  if (!(inv_temp > 0.f) || !std::isfinite(inv_temp))
+    return fail(KVR_EINVAL, "inv_temp must be positive and finite (got %g)", (double)inv_temp);
   *p = kvr::EntropyParams{};
   p->logits = logits; p->dtype = dtype; p->R = R; p->V = V; p->ld = ld; p->inv_temp = inv_temp; p->H = H;
   if (det) {

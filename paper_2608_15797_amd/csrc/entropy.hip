@@ -99,22 +99,64 @@ __device__ __forceinline__ rsrc_t row_rsrc(const void *p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-// Vector v (8 logits) of a row through its buffer resource, scaled by c.
-__device__ __forceinline__ void load8(rsrc_t r, int v, float c, float (&y)[8], const bf16_t *) {
-  const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 16u, 0, 0);
-  y[0] = bf16_lo(w.x) * c; y[1] = bf16_hi(w.x) * c;
-  y[2] = bf16_lo(w.y) * c; y[3] = bf16_hi(w.y) * c;
-  y[4] = bf16_lo(w.z) * c; y[5] = bf16_hi(w.z) * c;
-  y[6] = bf16_lo(w.w) * c; y[7] = bf16_hi(w.w) * c;
-}
+// Eight logits of a row, held as the raw loaded words until they are used, so
+// that a round's loads cost 4 (bf16) or 8 (fp32) registers per vector.
+template <typename T>
+struct Vec8;
+template <>
+struct Vec8<bf16_t> {
+  u32x4 w;
+  __device__ __forceinline__ void load(rsrc_t r, int v) {
+    w = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 16u, 0, 0);
+  }
+  __device__ __forceinline__ void get(float (&y)[8]) const {
+    y[0] = bf16_lo(w.x); y[1] = bf16_hi(w.x); y[2] = bf16_lo(w.y); y[3] = bf16_hi(w.y);
+    y[4] = bf16_lo(w.z); y[5] = bf16_hi(w.z); y[6] = bf16_lo(w.w); y[7] = bf16_hi(w.w);
+  }
+};
+template <>
+struct Vec8<float> {
+  u32x4 a, b;
+  __device__ __forceinline__ void load(rsrc_t r, int v) {
+    a = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u, 0, 0);
+    b = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u + 16u, 0, 0);
+  }
+  __device__ __forceinline__ void get(float (&y)[8]) const {
+    y[0] = __uint_as_float(a.x); y[1] = __uint_as_float(a.y); y[2] = __uint_as_float(a.z); y[3] = __uint_as_float(a.w);
+    y[4] = __uint_as_float(b.x); y[5] = __uint_as_float(b.y); y[6] = __uint_as_float(b.z); y[7] = __uint_as_float(b.w);
+  }
+};
 
-__device__ __forceinline__ void load8(rsrc_t r, int v, float c, float (&y)[8], const float *) {
-  const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u, 0, 0);
-  const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u + 16u, 0, 0);
-  y[0] = __uint_as_float(a.x) * c; y[1] = __uint_as_float(a.y) * c;
-  y[2] = __uint_as_float(a.z) * c; y[3] = __uint_as_float(a.w) * c;
-  y[4] = __uint_as_float(b.x) * c; y[5] = __uint_as_float(b.y) * c;
-  y[6] = __uint_as_float(b.z) * c; y[7] = __uint_as_float(b.w) * c;
+// The triple's reference m may trail the running maximum by up to this much
+// (log2 units, a factor of 256): every term 2^(y - m) stays finite and exact
+// to fp32 rounding, and the rescale is skipped for almost every vector once
+// the first few have been seen. The entropy does not depend on m.
+constexpr float kSlack = 8.0f;
+
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// Fold eight raw logits x into the triple, y = c * x with c > 0.
+__device__ __forceinline__ void tri_fold8(Tri &t, const float (&x)[8], float c) {
+  // NaN-propagating maximum: no operand canonicalisation, three-input
+  // instructions (NaN logits are unsupported anyway).
+  const float lm = vmax(vmax(vmax(x[0], x[1]), vmax(x[2], x[3])), vmax(vmax(x[4], x[5]), vmax(x[6], x[7]))) * c;
+  if (lm > t.m + kSlack) {
+    if (t.z > 0.f) {
+      const float f = fast_exp2(t.m - lm);
+      t.s = (t.s + (t.m - lm) * t.z) * f;
+      t.z *= f;
+    }
+    t.m = lm;
+  }
+  const float nm = -t.m;
+#pragma unroll
+  for (int e = 0; e < 8; e++) {
+    // Clamp keeps -inf logits (and -inf - (-inf)) finite so 0 * d stays 0.
+    const float d = fmaxf(fmaf(x[e], c, nm), -256.0f);
+    const float w = fast_exp2(d);
+    t.z += w;
+    t.s = fmaf(d, w, t.s);
+  }
 }
 
 __device__ __forceinline__ float load1(const bf16_t *ptr) { return bf16_to_f32(*ptr); }
@@ -124,17 +166,26 @@ __device__ __forceinline__ float finish_entropy(Tri t) {
   return kLn2 * (log2f(t.z) - t.s / t.z);
 }
 
-__device__ void detector_push(const EntropyParams &p, int row, float H) {
+// Detector update of one row by one whole wave (every lane passes the same
+// H): the history entries are read by the lanes in parallel, the new entry
+// taking its slot in registers, and summed with a wave reduction.
+__device__ void detector_push(const EntropyParams &p, int row, float H, int lane) {
   if (!p.hist) return;
+  float *h = p.hist + (size_t)row * p.window;
   const int c = p.cnt[row];
-  p.hist[(size_t)row * p.window + (c % p.window)] = H;
+  const int slot = c % p.window;
   const int c1 = c + 1;
-  p.cnt[row] = c1;
-  if (c1 >= p.guard) {
-    const int k = c1 < p.window ? c1 : p.window;
-    float sum = 0.f;
-    for (int i = 0; i < k; i++) sum += p.hist[(size_t)row * p.window + i];
-    if (sum / (float)k > p.tau) p.flag[row] = 1;
+  const int k = c1 < p.window ? c1 : p.window;
+  const bool judge = c1 >= p.guard;
+  float sum = 0.f;
+  if (judge) {
+    for (int i = lane; i < k; i += kWave) sum += i == slot ? H : h[i];
+    sum = wave_sum(sum);
+  }
+  if (lane == 0) {
+    h[slot] = H;
+    p.cnt[row] = c1;
+    if (judge && sum / (float)k > p.tau) p.flag[row] = 1;
   }
 }
 
@@ -342,10 +393,11 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
 
   Tri t{kNegInf, 0.f, 0.f};
   if constexpr (VEC) {
-    // U vectors of 8 logits per thread per round, all loads issued first.
-    // Entropy alone: 10, so that a split of the 7B / 1.5B vocabularies over 8
-    // workgroups per row is one round (measured 22% faster than 8). With the
-    // sampler: 8, whose lower register count keeps 4 waves per SIMD.
+    // U vectors of 8 logits per thread per round, all loads issued first and
+    // each vector folded as soon as it has arrived, so the arithmetic of the
+    // round overlaps its later loads. Entropy alone: 10, so that a split of
+    // the 7B / 1.5B vocabularies over 8 workgroups per row is one round. With
+    // the sampler: 8, whose lower register count keeps 4 waves per SIMD.
     constexpr int U = SAMPLE ? 8 : 10;
     const int nvec = p.V / 8;
     const int per = (nvec + splits - 1) / splits;
@@ -355,59 +407,45 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
     // partly used round load nothing instead of fetching the next split.
     const rsrc_t rr = row_rsrc(x, (uint32_t)v1 * 8u * (uint32_t)sizeof(T));
     // The loop bound is the same for every thread (lanes past the end load
-    // zeros and mask them), so waves offer sampler candidates in lockstep.
+    // zeros and skip them), so waves offer sampler candidates in lockstep.
     for (int b0 = v0; b0 < v1; b0 += U * kThreads) {
       const int base = b0 + tid;
-      float y[U][8];
+      const bool full = b0 + U * kThreads <= v1;
+      // The loads are issued in vector order (the scheduling barriers keep
+      // the compiler from reordering them), so that each fold below waits
+      // only for its own vector; the asm statement keeps a load whose value
+      // is used under a branch from sinking into it.
+      Vec8<T> w[U];
 #pragma unroll
-      for (int u = 0; u < U; u++) load8(rr, base + u * kThreads, SAMPLE ? 1.0f : c, y[u], x);
+      for (int u = 0; u < U; u++) {
+        w[u].load(rr, base + u * kThreads);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      asm volatile("" ::: "memory");
       if constexpr (SAMPLE) {
         if (b0 == v0) {
           // First round: seed the thresholds from the lanes' maxima.
           float mx = kNegInf;
 #pragma unroll
-          for (int u = 0; u < U; u++)
+          for (int u = 0; u < U; u++) {
+            float a[8];
+            w[u].get(a);
             if (base + u * kThreads < v1)
 #pragma unroll
-              for (int e = 0; e < 8; e++) mx = fmaxf(mx, y[u][e]);
+              for (int e = 0; e < 8; e++) mx = vmax(mx, a[e]);
+          }
           cand_seed(cs, mx, p.top_k);
-        }
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-          const int v = base + u * kThreads;
-          cand_offer(cs, p.top_k, lane, y[u], (uint32_t)v * 8u, v < v1 ? 8 : 0);
-#pragma unroll
-          for (int e = 0; e < 8; e++) y[u][e] *= c;
         }
       }
 #pragma unroll
       for (int u = 0; u < U; u++) {
-        const bool ok = base + u * kThreads < v1;
-#pragma unroll
-        for (int e = 0; e < 8; e++) y[u][e] = ok ? y[u][e] : kNegInf;
+        float a[8];
+        w[u].get(a);
+        const int v = base + u * kThreads;
+        const bool ok = full || v < v1;
+        if constexpr (SAMPLE) cand_offer(cs, p.top_k, lane, a, (uint32_t)v * 8u, ok ? 8 : 0);
+        if (ok) tri_fold8(t, a, c);
       }
-      float lm = kNegInf;
-#pragma unroll
-      for (int u = 0; u < U; u++)
-#pragma unroll
-        for (int e = 0; e < 8; e++) lm = fmaxf(lm, y[u][e]);
-      if (lm > t.m) {
-        if (t.z > 0.f) {
-          const float f = fast_exp2(t.m - lm);
-          t.s = (t.s + (t.m - lm) * t.z) * f;
-          t.z *= f;
-        }
-        t.m = lm;
-      }
-#pragma unroll
-      for (int u = 0; u < U; u++)
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-          const float d = fmaxf(y[u][e] - t.m, -256.0f);
-          const float w = fast_exp2(d);
-          t.z += w;
-          t.s = fmaf(d, w, t.s);
-        }
     }
     if (split == splits - 1) {
       // The V % 8 trailing logits (one per thread of the first wave).
@@ -472,40 +510,50 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
       Tri r = part[0];
 #pragma unroll
       for (int w = 1; w < NW; w++) r = tri_merge(r, part[w]);
-      float *mine_t = static_cast<float *>(p.ws) + ((size_t)row * splits + split) * 4;
-      mine_t[0] = r.m;
-      mine_t[1] = r.z;
-      mine_t[2] = r.s;
+      reinterpret_cast<float4 *>(p.ws)[(size_t)row * splits + split] = make_float4(r.m, r.z, r.s, 0.f);
     }
     return;
   } else {
-    if (tid != 0) return;
+    if (wave != 0) return;
     Tri r = part[0];
 #pragma unroll
     for (int w = 1; w < kThreads / kWave; w++) r = tri_merge(r, part[w]);
     if (splits == 1) {
       const float H = finish_entropy(r);
-      p.H[row] = H;
-      detector_push(p, row, H);
+      if (lane == 0) p.H[row] = H;
+      detector_push(p, row, H, lane);
       return;
     }
-    float *mine = static_cast<float *>(p.ws) + ((size_t)row * splits + split) * 4;
-    mine[0] = r.m;
-    mine[1] = r.z;
-    mine[2] = r.s;
+    if (lane == 0)
+      reinterpret_cast<float4 *>(p.ws)[(size_t)row * splits + split] = make_float4(r.m, r.z, r.s, 0.f);
   }
 }
 
-// Per-row merge of the split partials, then the detector; one thread per row.
-__global__ __launch_bounds__(256) void entropy_merge(EntropyParams p) {
-  const int row = blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= p.R) return;
-  const float *q = static_cast<const float *>(p.ws) + (size_t)row * p.splits * 4;
+// The merged triple of a row's split partials ([splits] float4 (m, Z, S, -)
+// in the workspace), by one whole wave: each lane loads every 64th partial,
+// so the row costs one memory round trip.
+__device__ __forceinline__ Tri wave_merge_splits(const EntropyParams &p, int row, int lane) {
+  const float4 *q = reinterpret_cast<const float4 *>(p.ws) + (size_t)row * p.splits;
   Tri acc{kNegInf, 0.f, 0.f};
-  for (int k = 0; k < p.splits; k++) acc = tri_merge(acc, Tri{q[4 * k], q[4 * k + 1], q[4 * k + 2]});
-  const float H = finish_entropy(acc);
-  p.H[row] = H;
-  detector_push(p, row, H);
+  for (int k = lane; k < p.splits; k += kWave) {
+    const float4 v = q[k];
+    acc = tri_merge(acc, Tri{v.x, v.y, v.z});
+  }
+#pragma unroll
+  for (int msk = 32; msk >= 1; msk >>= 1) {
+    Tri o{shfl_xor(acc.m, msk), shfl_xor(acc.z, msk), shfl_xor(acc.s, msk)};
+    acc = tri_merge(acc, o);
+  }
+  return acc;
+}
+
+// Per-row merge of the split partials, then the detector; one wave per row.
+__global__ __launch_bounds__(kWave) void entropy_merge(EntropyParams p) {
+  const int row = blockIdx.x;
+  const int lane = threadIdx.x;
+  const float H = finish_entropy(wave_merge_splits(p, row, lane));
+  if (lane == 0) p.H[row] = H;
+  detector_push(p, row, H, lane);
 }
 
 constexpr int kMergeEntries = 1024;  // splits * top_k bound of the sampling merge
@@ -519,19 +567,9 @@ __global__ __launch_bounds__(kWave) void sample_merge(EntropyParams p) {
   const int row = blockIdx.x;
   const int lane = threadIdx.x;
   const int S = p.splits, K = p.top_k;
-  const float *q = static_cast<const float *>(p.ws) + (size_t)row * S * 4;
-  Tri acc{kNegInf, 0.f, 0.f};
-  for (int k = lane; k < S; k += kWave) acc = tri_merge(acc, Tri{q[4 * k], q[4 * k + 1], q[4 * k + 2]});
-#pragma unroll
-  for (int msk = 32; msk >= 1; msk >>= 1) {
-    Tri o{shfl_xor(acc.m, msk), shfl_xor(acc.z, msk), shfl_xor(acc.s, msk)};
-    acc = tri_merge(acc, o);
-  }
-  if (lane == 0) {
-    const float H = finish_entropy(acc);
-    p.H[row] = H;
-    detector_push(p, row, H);
-  }
+  const float H = finish_entropy(wave_merge_splits(p, row, lane));
+  if (lane == 0) p.H[row] = H;
+  detector_push(p, row, H, lane);
   // Candidates.
   const uint64_t *keys = reinterpret_cast<const uint64_t *>(static_cast<const float *>(p.ws) +
                                                             (size_t)p.R * S * 4) + (size_t)row * S * K;
@@ -645,7 +683,7 @@ hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream) {
     return hipGetLastError();
   }
   if (p.splits == 1) return e;
-  hipLaunchKernelGGL(entropy_merge, dim3((p.R + 255) / 256), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL(entropy_merge, dim3(p.R), dim3(kWave), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -76,6 +76,10 @@ def test_entropy_rejects_bad_arguments_on_host():
     need = kvr.lib.kvr_logit_entropy_workspace_size(8, 151936)
     assert need > 0
     assert kvr.lib.kvr_logit_entropy(16, 1, 8, 151936, 151936, 1.0, 16, None, None, 0, None) == -4
+    # The softmax temperature's inverse must be positive and finite.
+    for bad in (0.0, -1.0, float("inf"), float("nan")):
+        assert kvr.lib.kvr_logit_entropy(16, 1, 4, 10, 10, bad, 16, None, None, 0, None) == -1
+        assert "inv_temp" in kvr.lib.kvr_last_error().decode()
 
 
 def test_prefix_workspace_size_matches_split_plan():
