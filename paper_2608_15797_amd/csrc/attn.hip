@@ -311,19 +311,12 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   const bf16_t *kn = p.k_new ? static_cast<const bf16_t *>(p.k_new) + (size_t)unit * D : nullptr;
   const bf16_t *vn = p.v_new ? static_cast<const bf16_t *>(p.v_new) + (size_t)unit * D : nullptr;
   const bool append = kn != nullptr && n >= 1;
-
-  // Append the new token at slot n-1 (reads below take it from k_new/v_new).
-  if (append) {
-    constexpr int LPR = D / 8;  // lanes per row, 16 bytes each
-    if (lane < LPR) {
-      reinterpret_cast<u32x4 *>(Kc + (size_t)(n - 1) * D)[lane] = reinterpret_cast<const u32x4 *>(kn)[lane];
-    } else if (lane < 2 * LPR) {
-      const int i = lane - LPR;
-      reinterpret_cast<u32x4 *>(Vc + (size_t)(n - 1) * D)[i] = reinterpret_cast<const u32x4 *>(vn)[i];
-    } else if (lane == 2 * LPR && p.pos && p.new_pos) {
-      p.pos[(size_t)unit * p.cap + n - 1] = p.new_pos[s];
-    }
-  }
+  // The new token goes to slot n-1. Its K and V rows are loaded once, as the
+  // one-key tile below, and written to the cache from those registers once
+  // the unit's other loads are in flight, so no load-to-store round trip
+  // precedes them. Reads of the cache stop at slot n-2.
+  const bool put_pos = append && p.pos != nullptr && p.new_pos != nullptr;
+  const int32_t npos = put_pos ? p.new_pos[s] : 0;
   const int ncache = append ? n - 1 : n;
 
   const int qh0 = h * G;
@@ -398,6 +391,22 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   float xnew = kNegInf;  // the new token's logit, stored after the tail chunk's masked ones
   auto new_token = [&]() {
     if (append) {
+      // Cache rows of the new token from the tile's registers: K row 0 is held
+      // by the lanes with r16 == 0 (d = 32i + 8 g4), V row 0 by the lanes with
+      // g4 == 0 (d = r16 D/16).
+      if (r16 == 0) {
+#pragma unroll
+        for (int i = 0; i < Geo<D>::NLD; i++)
+          *reinterpret_cast<u32x4 *>(Kc + (size_t)(n - 1) * D + 32 * i + 8 * g4) = cn.k[0][i];
+      }
+      if (g4 == 0) {
+        bf16_t *vd = Vc + (size_t)(n - 1) * D + r16 * NB;
+        if constexpr (D == 128)
+          *reinterpret_cast<u32x4 *>(vd) = u32x4{cn.v[0][0][0], cn.v[0][0][1], cn.v[0][0][2], cn.v[0][0][3]};
+        else
+          *reinterpret_cast<u32x2 *>(vd) = u32x2{cn.v[0][0][0], cn.v[0][0][1]};
+      }
+      if (put_pos && lane == 16) p.pos[(size_t)unit * p.cap + n - 1] = npos;
       float x[1][4];
       chunk_logits<D, 1>(cn, qop, x, 0, 1, g4, sl2, true);
       xnew = x[0][0];
@@ -439,7 +448,13 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
           const float w = mk == kNegInf ? 0.0f : fast_exp2(mk - M);
           zi += r[1] * w;
 #pragma unroll
-          for (int b = 0; b < NB; b++) o[b][i] += r[4 + r16 * NB + b] * w;
+          for (int b = 0; b < NB; b += 4) {
+            const float4_t x = *reinterpret_cast<const float4_t *>(r + 4 + r16 * NB + b);
+            o[b][i] += x[0] * w;
+            o[b + 1][i] += x[1] * w;
+            o[b + 2][i] += x[2] * w;
+            o[b + 3][i] += x[3] * w;
+          }
         }
       }
     }
@@ -501,6 +516,13 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
   const int g4 = lane >> 4;
   const int G = p.G;
   const int rows = p.C * G;
+  // Records of the wave's first segment when more follow: [rows][D + 4]
+  // floats in LDS, written to the workspace once the span is done. Stores
+  // to HBM in the middle of a wave's read stream cost far more than their
+  // bytes (measured: about 6% of the kernel's time), so every record store
+  // waits for the end of the wave.
+  extern __shared__ float deferred[];
+  int dunit = -1, dsplit = 0;
 
   // This wave's keys [g0, g1) of the flattened (unit, key) space, one segment
   // per unit it touches; each segment leaves one partial record per row.
@@ -567,7 +589,13 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
   };
   stream_chunks<D, TILES, DEPTH>(Kr, Vr, k0, k1, r16, g4, [] {}, process);
 
-  float *ws = p.ws;
+  // The segment's records: to LDS if it is the first of several, else to
+  // the workspace.
+  const bool defer = dunit < 0 && g < g1;
+  if (defer) {
+    dunit = unit;
+    dsplit = split;
+  }
 #pragma unroll
   for (int rb = 0; rb < RB; rb++) {
     float z = st[rb].zl;
@@ -580,17 +608,44 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
       const float zi = __shfl(z, rl, kWave);
       const int rho = rb * 16 + rl;
       if (rho < rows) {
-        const int c = rho / G, g = rho % G;
-        const int s = pp * p.C + c;
-        const size_t rec = (((size_t)split * p.S + s) * p.L + l) * p.Hq + h * G + g;
-        float *r = ws + rec * (D + 4);
-        if (r16 == 0) { r[0] = mi; r[1] = zi; }
+        // 16-byte stores: the lane's NB consecutive columns of the row (a
+        // record is D + 4 floats, so every record and its o part are 16-byte
+        // aligned), and (max, sum) from the first lane of the row.
+        auto put = [&](float *r) {
+          if (r16 == 0) *reinterpret_cast<float2_t *>(r) = float2_t{mi, zi};
 #pragma unroll
-        for (int b = 0; b < NB; b++) r[4 + r16 * NB + b] = o[rb][b][i];
+          for (int b = 0; b < NB; b += 4)
+            *reinterpret_cast<float4_t *>(r + 4 + r16 * NB + b) =
+                float4_t{o[rb][b][i], o[rb][b + 1][i], o[rb][b + 2][i], o[rb][b + 3][i]};
+        };
+        if (defer) {
+          put(deferred + (size_t)rho * (D + 4));
+        } else {
+          const int c = rho / G, g = rho % G;
+          const int s = pp * p.C + c;
+          put(p.ws + ((((size_t)split * p.S + s) * p.L + l) * p.Hq + h * G + g) * (D + 4));
+        }
       }
     }
   }
   }  // segments
+
+  // Write out the deferred records: the G records of a candidate are
+  // contiguous in the workspace (record ((split * S + s) * L + l) * Hq + h G + g).
+  if (dunit >= 0) {
+    __syncthreads();
+    const int h = dunit % p.Hkv;
+    const int pl = dunit / p.Hkv;
+    const int l = pl % p.L;
+    const int pp = pl / p.L;
+    const int per_c = G * (D + 4) / 4;  // float4s per candidate
+    const float4_t *src = reinterpret_cast<const float4_t *>(deferred);
+    for (int u = lane; u < p.C * per_c; u += kWave) {
+      const int c = u / per_c;
+      const size_t rec0 = (((size_t)dsplit * p.S + pp * p.C + c) * p.L + l) * p.Hq + h * G;
+      reinterpret_cast<float4_t *>(p.ws + rec0 * (D + 4))[u - c * per_c] = src[u];
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -685,6 +740,12 @@ __global__ __launch_bounds__(64) void attn_f32(AttnParams p, int nt_max) {
   }
 }
 
+// LDS of a context-kernel wave: the deferred records of RB * 16 rows.
+template <int D>
+size_t prefix_lds_bytes(int rb) {
+  return (size_t)rb * 16 * (D + 4) * sizeof(float);
+}
+
 template <int D>
 hipError_t launch_bf16(const AttnParams &p_in, hipStream_t stream) {
   AttnParams p = p_in;
@@ -704,11 +765,12 @@ hipError_t launch_bf16(const AttnParams &p_in, hipStream_t stream) {
   // Context splits first; the suffix kernel then merges their partials.
   const int rb = (p.C * p.G + 15) / 16;
   const dim3 gridA(p.nwaves);
+  const size_t lds = prefix_lds_bytes<D>(rb);
   switch (rb) {
-    case 1: hipLaunchKernelGGL((attn_prefix_bf16<D, 1, 2, 2>), gridA, dim3(64), 0, stream, p); break;
-    case 2: hipLaunchKernelGGL((attn_prefix_bf16<D, 2, 2, 2>), gridA, dim3(64), 0, stream, p); break;
-    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3, 1, 2>), gridA, dim3(64), 0, stream, p); break;
-    case 4: hipLaunchKernelGGL((attn_prefix_bf16<D, 4, 1, 2>), gridA, dim3(64), 0, stream, p); break;
+    case 1: hipLaunchKernelGGL((attn_prefix_bf16<D, 1, 2, 2>), gridA, dim3(64), lds, stream, p); break;
+    case 2: hipLaunchKernelGGL((attn_prefix_bf16<D, 2, 2, 2>), gridA, dim3(64), lds, stream, p); break;
+    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3, 1, 2>), gridA, dim3(64), lds, stream, p); break;
+    case 4: hipLaunchKernelGGL((attn_prefix_bf16<D, 4, 1, 2>), gridA, dim3(64), lds, stream, p); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
@@ -737,8 +799,9 @@ int prefix_slots() {
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     cus = 256;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_prefix_bf16<D, RB, TILES, 2>, 64, 0) !=
-          hipSuccess || per_cu <= 0)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_prefix_bf16<D, RB, TILES, 2>, 64,
+                                                    prefix_lds_bytes<D>(RB)) != hipSuccess ||
+      per_cu <= 0)
     per_cu = 4;
   v = cus * per_cu;
   cached.store(v, std::memory_order_relaxed);

@@ -157,6 +157,7 @@ PREFIX_CASES = [
     (8, 2, 1, 2, 8, 128, 2100, 33, torch.bfloat16),   # 4 x 8 = 32 rows
     (8, 1, 1, 1, 8, 128, 300, 16, torch.bfloat16),    # 8 x 8 = 64 rows
     (6, 3, 2, 2, 6, 64, 513, 20, torch.bfloat16),
+    (8, 2, 2, 2, 6, 128, 150, 24, torch.bfloat16),    # spans of 512 keys cross up to 4 units
     (4, 2, 1, 2, 6, 128, 200, 24, torch.float32),
 ]
 
