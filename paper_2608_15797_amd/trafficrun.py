@@ -1,0 +1,71 @@
+"""Program for the HBM byte-counter passes of the attention and eviction calls.
+
+    python -m paper_2608_15797_amd.trafficrun [--workload NAME] [--steps N]
+
+Runs a calibration copy (three dispatches of a 1 GiB bf16 -> fp16 conversion:
+1 GiB read and 1 GiB written each, the reference that profsum scales the
+FETCH_SIZE / WRITE_SIZE counters by), then the workload's prompt and N decode
+steps of base attention (with its evictions) and helper attention, the calls
+of the decode step that move more than 99% of its bytes. The entropy calls
+are left out of these passes; their bytes are measured on their own.
+Run it under one `rocprofv3 --pmc FETCH_SIZE` and one `--pmc WRITE_SIZE` pass
+and give both result directories to `profsum --traffic`. N defaults to the
+workload's decode steps, the benchmark's timed window, so the per-dispatch
+averages cover the same mix of cache and suffix lengths (the prompt adds the
+same few hundred dispatches as in the benchmark's own run).
+"""
+from __future__ import annotations
+
+import argparse
+import sys
+import time
+
+import torch
+
+
+def calibration_copy(nbytes: int = 1 << 30) -> None:
+    # A conversion runs as a kernel; a same-type copy may go to a DMA engine
+    # that the counters do not see.
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty(nbytes // 2, dtype=torch.float16, device="cuda")
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
+
+
+def main(argv=None) -> None:
+    from paper_2608_15797_amd.pipeline import Decoder
+    from paper_2608_15797_amd.workloads import WORKLOADS
+
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--workload", default="base7b_helper", choices=sorted(WORKLOADS))
+    ap.add_argument("--steps", type=int, default=0, help="decode steps (default: the workload's)")
+    args = ap.parse_args(argv)
+    calibration_copy()
+    print("calibration copy done", flush=True)
+    wl = WORKLOADS[args.workload]
+    if args.steps:
+        wl = wl.with_(steps=args.steps)
+    t0 = time.time()
+    dec = Decoder(wl, device="cuda")
+    dec.prompt()
+    torch.cuda.synchronize()
+    print("[%s] prompt (%d tokens) done" % (wl.name, dec.T_prompt), flush=True)
+    for i in range(wl.steps):
+        t = dec.T_prompt + i
+        si = dec.inputs(t)
+        if wl.base:
+            dec.base_token(t, si)
+        if wl.helper:
+            dec.helper_token(i, si)
+        if (i + 1) % 512 == 0:
+            torch.cuda.synchronize()
+            print("[%s] %d steps (%.1fs)" % (wl.name, i + 1, time.time() - t0), flush=True)
+    torch.cuda.synchronize()
+    print("done", flush=True)
+
+
+if __name__ == "__main__":
+    sys.exit(main())
