@@ -36,7 +36,7 @@ from paper_2608_15797_amd.workloads import WORKLOADS  # noqa: E402
 
 PEAK_HBM_GBPS = 8000.0
 METRIC = "candidate decode steps/s (attn+evict+entropy)"
-DEFAULT_EXTRA = ("base7b", "base72b_helper")
+DEFAULT_EXTRA = ("base7b", "base72b_helper", "helper4k")
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
