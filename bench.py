@@ -41,15 +41,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def step_bytes(wl, dec, i):
-    """Algorithmic bytes of decode step i by call name."""
+def step_bytes(wl, dec, i, moved_rows=None):
+    """Algorithmic bytes of decode step i by call name. moved_rows: kept rows
+    per head that change slot at an eviction, on average (None = all B, the
+    upper bound)."""
     out = {}
     if wl.base:
         b = wl.base
         n = dec.blen_host[dec.T_prompt + i]
         out["base_attn"] = acc.base_attn_bytes(wl, n)
         if n > b.B + b.buffer:
-            out["evict"] = acc.evict_bytes(wl, n)
+            out["evict"] = acc.evict_bytes(wl, n, moved_rows)
     if wl.helper:
         out["helper_attn"] = acc.helper_attn_bytes(wl, dec.hlen_host[i])
     e = acc.esize(wl)
@@ -84,22 +86,25 @@ def run_workload(name, steps, warmup, instrument=True):
     ms = start.elapsed_time(end)
     log("[%s] timed %d steps: %.3f ms/step" % (name, steps, ms / steps))
 
-    total = {}
-    for i in range(warmup, warmup + steps):
-        for k, v in step_bytes(wl, dec, i).items():
-            total[k] = total.get(k, 0) + v
-    all_bytes = sum(total.values())
-
     calls = {}
+    moved_rows = None
     if instrument:
-        timers = {}
+        # Per-call durations from event pairs around every call. The kept sets
+        # of each eviction are read back after it (outside the event pairs) to
+        # count the rows that changed slot: eviction's algorithmic bytes.
+        timers, moved = {}, []
         for i in range(warmup + steps, warmup + 2 * steps):
-            dec.step(i, timers=timers)
+            dec.step(i, timers=timers, evict_log=moved)
         torch.cuda.synchronize()
-        ibytes = {}
+        if moved:
+            b = wl.base
+            moved_rows = sum(moved) / len(moved) / (b.S * b.L * b.Hkv)
+        ibytes, ubound = {}, {}
         for i in range(warmup + steps, warmup + 2 * steps):
-            for k, v in step_bytes(wl, dec, i).items():
+            for k, v in step_bytes(wl, dec, i, moved_rows).items():
                 ibytes[k] = ibytes.get(k, 0) + v
+            for k, v in step_bytes(wl, dec, i).items():
+                ubound[k] = ubound.get(k, 0) + v
         for k, ev in timers.items():
             dur = [s.elapsed_time(e) for s, e in ev]
             n = len(dur)
@@ -109,7 +114,19 @@ def run_workload(name, steps, warmup, instrument=True):
                             bytes_per_call=int(b_per),
                             GBps=round(b_per / (avg_ms * 1e-3) / 1e9, 1),
                             frac=round(b_per / (avg_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4))
+            if k == "evict":
+                ub = ubound[k] / n
+                calls[k].update(moved_rows_per_head=round(moved_rows, 2), bytes_upper_bound=int(ub),
+                                frac_upper_bound=round(ub / (avg_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4))
         log("[%s] per-call: %s" % (name, json.dumps(calls)))
+
+    # Whole-step algorithmic bytes of the timed window (eviction at the moved
+    # rows measured above, else at the upper bound).
+    total = {}
+    for i in range(warmup, warmup + steps):
+        for k, v in step_bytes(wl, dec, i, moved_rows).items():
+            total[k] = total.get(k, 0) + v
+    all_bytes = sum(total.values())
 
     S = (wl.base.S if wl.base else 0) + (wl.helper.S if wl.helper else 0)
     res = dict(workload=name, steps=steps, ms_per_step=ms / steps,

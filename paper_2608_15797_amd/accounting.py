@@ -44,12 +44,13 @@ def base_attn_flops(wl: Workload, n: int) -> int:
     return 4 * b.D * n * b.S * b.L * b.Hq
 
 
-def evict_bytes(wl: Workload, n: int, moved_rows: int | None = None) -> int:
-    """moved_rows: kept rows per head that change slot (None = all B)."""
+def evict_bytes(wl: Workload, n: int, moved_rows: float | None = None) -> int:
+    """moved_rows: kept rows per head that change slot, on average over the
+    heads (None = the upper bound, all B)."""
     b, e = wl.base, esize(wl)
     heads = b.S * b.L * b.Hkv
     m = b.B if moved_rows is None else moved_rows
-    return heads * ((n - b.W) * 4 + m * 2 * (2 * b.D * e + 4))
+    return int(heads * ((n - b.W) * 4 + m * 2 * (2 * b.D * e + 4)))
 
 
 def helper_attn_bytes(wl: Workload, u: int) -> int:

@@ -10,11 +10,14 @@
 // always kept.
 //
 // Compaction: kept slot k_i moves to slot i. Since k_i >= i, destinations are
-// processed in ascending chunks of 16 rows: all sources of a chunk are read
-// into registers, the workgroup synchronises, then the chunk is written. A
-// chunk's writes land on rows below every later chunk's sources, so nothing is
-// overwritten before it is read. Rows already in place (the kept prefix before
-// the first evicted slot) are not touched.
+// processed in ascending chunks of one 16-byte item of K and one of V per
+// thread (16 rows of bf16 D = 128): all sources of a chunk are read into
+// registers, the reads are waited for, the workgroup synchronises, then the
+// chunk is written. A chunk's writes land on rows below every later chunk's
+// sources, so nothing is overwritten before it is read. Rows already in place
+// (the kept prefix before the first evicted slot) are not touched. Larger
+// chunks (up to 128 rows per read phase) measured slower: the registers they
+// hold cut the number of heads in flight, which is what hides the latency.
 #include <hip/hip_runtime.h>
 
 #include "kvr_device.h"
@@ -32,8 +35,7 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 }
 
 constexpr int kThreads = 256;
-constexpr int kChunk = 16;
-constexpr int kMaxItems = 2;  // per thread per chunk: kChunk * (row bytes / 16) <= 512
+constexpr int kItems = 1;  // 16-byte items per thread per tensor per chunk
 
 __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int row_units) {
   extern __shared__ uint32_t lds[];
@@ -88,35 +90,39 @@ __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int
   char *Kb = static_cast<char *>(p.k) + (size_t)unit * p.cap * row_bytes;
   char *Vb = static_cast<char *>(p.v) + (size_t)unit * p.cap * row_bytes;
   int32_t *pos = p.pos ? p.pos + (size_t)unit * p.cap : nullptr;
-  const int items = kChunk * row_units;
+  const int chunk_rows = kThreads * kItems / row_units;  // <= kThreads (row_units >= 8)
   // first_moved is uniform; start at the chunk holding it.
-  for (int c0 = first_moved; c0 < p.B; c0 += kChunk) {
-    u32x4 kr[kMaxItems], vr[kMaxItems];
+  for (int c0 = first_moved; c0 < p.B; c0 += chunk_rows) {
+    u32x4 kr[kItems], vr[kItems];
     int32_t pr = 0;
 #pragma unroll
-    for (int a = 0; a < kMaxItems; a++) {
-      const int e = tid + a * kThreads;
+    for (int a = 0; a < kItems; a++) {
+      const int e = tid + a * kThreads;  // item of the chunk: row e / row_units, 16 bytes e % row_units
       const int i = c0 + e / row_units;
-      if (e < items && i < p.B) {
+      if (i < p.B) {
         const int src = kept[i];
         const int u = e % row_units;
         kr[a] = reinterpret_cast<const u32x4 *>(Kb + (size_t)src * row_bytes)[u];
         vr[a] = reinterpret_cast<const u32x4 *>(Vb + (size_t)src * row_bytes)[u];
       }
     }
-    if (pos && tid < kChunk && c0 + tid < p.B) pr = pos[kept[c0 + tid]];
+    if (pos && tid < chunk_rows && c0 + tid < p.B) pr = pos[kept[c0 + tid]];
+    // Every read of the chunk is performed before any thread writes.
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 #pragma unroll
-    for (int a = 0; a < kMaxItems; a++) {
+    for (int a = 0; a < kItems; a++) {
       const int e = tid + a * kThreads;
       const int i = c0 + e / row_units;
-      if (e < items && i < p.B) {
+      if (i < p.B) {
         const int u = e % row_units;
         reinterpret_cast<u32x4 *>(Kb + (size_t)i * row_bytes)[u] = kr[a];
         reinterpret_cast<u32x4 *>(Vb + (size_t)i * row_bytes)[u] = vr[a];
       }
     }
-    if (pos && tid < kChunk && c0 + tid < p.B) pos[c0 + tid] = pr;
+    if (pos && tid < chunk_rows && c0 + tid < p.B) pos[c0 + tid] = pr;
+    // Later chunks read only rows above this chunk's destinations, so they
+    // need no wait for these writes.
   }
 }
 

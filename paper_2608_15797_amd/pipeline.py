@@ -154,10 +154,13 @@ class Decoder:
 
     # -- one token ------------------------------------------------------------
     def base_token(self, t: int, si: StepInputs, stream=None, on_scored=None,
-                   timers=None) -> bool:
+                   timers=None, evict_log=None) -> bool:
         """Append + attend (+ score) for token t; evict if the cache overflows.
         Returns True when an eviction ran. `on_scored(t)` (tests) runs between
-        the attention and the eviction."""
+        the attention and the eviction. With `evict_log` (a list), each
+        eviction appends the number of kept rows, over all heads, that changed
+        slot (read back from the kept sets: a synchronising copy, for
+        accounting outside timed regions)."""
         b = self.wl.base
         with _timer(timers, "base_attn", stream):
             kvr.decode_attn(self.bcache, self.blen[t], si.bq, self.bout, self.bscale,
@@ -169,6 +172,9 @@ class Decoder:
             with _timer(timers, "evict", stream):
                 kvr.evict_topb(self.bcache, self.blen[t], self.scores, self.policy,
                                kept=self.kept, stream=stream)
+            if evict_log is not None:
+                slot = torch.arange(b.B, dtype=torch.int32, device=self.kept.device)
+                evict_log.append(int((self.kept != slot).sum()))
             return True
         return False
 
@@ -190,14 +196,15 @@ class Decoder:
         for t in range(self.T_prompt):
             self.base_token(t, self.inputs(t), stream)
 
-    def step(self, step: int, stream=None, timers=None) -> None:
+    def step(self, step: int, stream=None, timers=None, evict_log=None) -> None:
         """Decode step `step` (0-based, after the prompt): the whole hot path.
         With `timers` (a dict), each call is bracketed by a pair of timing
-        events on the launch stream, appended under its name."""
+        events on the launch stream, appended under its name; `evict_log` as
+        for base_token."""
         t = self.T_prompt + step
         si = self.inputs(t)
         if self.wl.base:
-            self.base_token(t, si, stream, timers=timers)
+            self.base_token(t, si, stream, timers=timers, evict_log=evict_log)
         if self.wl.helper:
             self.helper_token(step, si, stream, timers=timers)
         self.entropy(si, stream, timers=timers)
