@@ -58,6 +58,21 @@ struct Geo {
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// A split-K partial record of one query row: (max, sum, -, -) as float32 in
+// the log2 domain, then o / sum as D float16 (the sum-normalised output, at
+// most max |v| in size), so 4 + D/2 float slots, a multiple of 16 bytes.
+template <int D>
+constexpr int kRecFloats = 4 + D / 2;
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2v_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2v_t){a, b}, half2_t));
+}
+__device__ __forceinline__ float f16_lo(uint32_t w) { return (float)__builtin_bit_cast(half2_t, w)[0]; }
+__device__ __forceinline__ float f16_hi(uint32_t w) { return (float)__builtin_bit_cast(half2_t, w)[1]; }
+
 __device__ __forceinline__ short4_t s4(uint32_t a, uint32_t b) {
   u32x2 v = {a, b};
   return __builtin_bit_cast(short4_t, v);
@@ -321,20 +336,21 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
 
   const int qh0 = h * G;
   // Merge: the partial records of this wave's rows, piece k at stride
-  // S*L*Hq*(D+4) floats, G contiguous records each. The first merge_pf pieces
+  // S*L*Hq records, G contiguous records each. The first merge_pf pieces
   // are copied into LDS now (buffer-to-LDS loads, 1 KiB per instruction) so
   // the epilogue does not wait on them.
+  constexpr int RF = kRecFloats<D>;
   int npieces = 0, pf = 0;
-  const size_t rstride = (size_t)p.S * p.L * p.Hq * (D + 4);
+  const size_t rstride = (size_t)p.S * p.L * p.Hq * RF;
   const float *rbase = nullptr;
   if constexpr (MERGE) {
     const long ug = ((long)((s / p.C) * p.L + l) * p.Hkv + h) * p.plen;
     npieces = (int)((ug + p.plen - 1) / p.span - ug / p.span) + 1;
     pf = npieces < p.merge_pf ? npieces : p.merge_pf;
-    rbase = p.ws + (((size_t)s * p.L + l) * p.Hq + qh0) * (D + 4);
+    rbase = p.ws + (((size_t)s * p.L + l) * p.Hq + qh0) * RF;
 #if defined(__HIP_DEVICE_COMPILE__)
     for (int k = 0; k < pf; k++) {
-      const rsrc_t rr = make_rsrc(rbase + k * rstride, (uint32_t)G * (D + 4) * 4u);
+      const rsrc_t rr = make_rsrc(rbase + k * rstride, (uint32_t)G * RF * 4u);
       for (int j = 0; j < p.merge_blk / 256; j++)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void_t *)(smem + k * p.merge_blk + j * 256), 16,
                                                  (uint32_t)(j * 1024 + lane * 16), 0, 0, 0);
@@ -428,13 +444,13 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
     float zi = __shfl(z, row, kWave);
     if constexpr (MERGE) {
       // Log-sum-exp merge with the context partials of this row:
-      // record = (max, sum, -, -, unnormalised o[D]) in the log2 domain.
+      // record = (max, sum, -, -, o[D] / sum) in the log2 domain.
       const float mi = __shfl(st.m, row, kWave);
       if (i == 0) wait_vm0();  // the LDS copies of the partials have landed
       if (row < G) {
         // Piece k of this row's record: in LDS for k < pf, else in the workspace.
         auto rec = [&](int k) -> const float * {
-          return k < pf ? smem + k * p.merge_blk + row * (D + 4) : rbase + k * rstride + row * (D + 4);
+          return k < pf ? smem + k * p.merge_blk + row * RF : rbase + k * rstride + row * RF;
         };
         float M = mi;
         for (int k = 0; k < npieces; k++) M = fmaxf(M, rec(k)[0]);
@@ -445,15 +461,21 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
         for (int k = 0; k < npieces; k++) {
           const float *r = rec(k);
           const float mk = r[0];
-          const float w = mk == kNegInf ? 0.0f : fast_exp2(mk - M);
-          zi += r[1] * w;
+          const float w = mk == kNegInf ? 0.0f : r[1] * fast_exp2(mk - M);
+          zi += w;
+          // The lane's NB columns: NB float16 at float slot 4 + r16 * NB / 2.
+          uint32_t hv[NB / 2];
+          if constexpr (D == 128) {
+            const u32x4 x = *reinterpret_cast<const u32x4 *>(r + 4 + r16 * (NB / 2));
+            hv[0] = x.x; hv[1] = x.y; hv[2] = x.z; hv[3] = x.w;
+          } else {
+            const u32x2 x = *reinterpret_cast<const u32x2 *>(r + 4 + r16 * (NB / 2));
+            hv[0] = x.x; hv[1] = x.y;
+          }
 #pragma unroll
-          for (int b = 0; b < NB; b += 4) {
-            const float4_t x = *reinterpret_cast<const float4_t *>(r + 4 + r16 * NB + b);
-            o[b][i] += x[0] * w;
-            o[b + 1][i] += x[1] * w;
-            o[b + 2][i] += x[2] * w;
-            o[b + 3][i] += x[3] * w;
+          for (int b = 0; b < NB / 2; b++) {
+            o[2 * b][i] += f16_lo(hv[b]) * w;
+            o[2 * b + 1][i] += f16_hi(hv[b]) * w;
           }
         }
       }
@@ -516,7 +538,7 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
   const int g4 = lane >> 4;
   const int G = p.G;
   const int rows = p.C * G;
-  // Records of the wave's first segment when more follow: [rows][D + 4]
+  // Records of the wave's first segment when more follow: [rows][4 + D/2]
   // floats in LDS, written to the workspace once the span is done. Stores
   // to HBM in the middle of a wave's read stream cost far more than their
   // bytes (measured: about 6% of the kernel's time), so every record store
@@ -608,22 +630,26 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
       const float zi = __shfl(z, rl, kWave);
       const int rho = rb * 16 + rl;
       if (rho < rows) {
-        // 16-byte stores: the lane's NB consecutive columns of the row (a
-        // record is D + 4 floats, so every record and its o part are 16-byte
-        // aligned), and (max, sum) from the first lane of the row.
+        // One store of the lane's NB consecutive columns of o / sum as
+        // float16 (16 bytes at D = 128; records are 16-byte multiples), and
+        // (max, sum) from the first lane of the row.
+        const float inv = zi > 0.f ? 1.0f / zi : 0.f;
         auto put = [&](float *r) {
           if (r16 == 0) *reinterpret_cast<float2_t *>(r) = float2_t{mi, zi};
+          uint32_t hv[NB / 2];
 #pragma unroll
-          for (int b = 0; b < NB; b += 4)
-            *reinterpret_cast<float4_t *>(r + 4 + r16 * NB + b) =
-                float4_t{o[rb][b][i], o[rb][b + 1][i], o[rb][b + 2][i], o[rb][b + 3][i]};
+          for (int b = 0; b < NB / 2; b++) hv[b] = pack_f16x2(o[rb][2 * b][i] * inv, o[rb][2 * b + 1][i] * inv);
+          if constexpr (D == 128)
+            *reinterpret_cast<u32x4 *>(r + 4 + r16 * (NB / 2)) = u32x4{hv[0], hv[1], hv[2], hv[3]};
+          else
+            *reinterpret_cast<u32x2 *>(r + 4 + r16 * (NB / 2)) = u32x2{hv[0], hv[1]};
         };
         if (defer) {
-          put(deferred + (size_t)rho * (D + 4));
+          put(deferred + (size_t)rho * kRecFloats<D>);
         } else {
           const int c = rho / G, g = rho % G;
           const int s = pp * p.C + c;
-          put(p.ws + ((((size_t)split * p.S + s) * p.L + l) * p.Hq + h * G + g) * (D + 4));
+          put(p.ws + ((((size_t)split * p.S + s) * p.L + l) * p.Hq + h * G + g) * kRecFloats<D>);
         }
       }
     }
@@ -638,12 +664,12 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
     const int pl = dunit / p.Hkv;
     const int l = pl % p.L;
     const int pp = pl / p.L;
-    const int per_c = G * (D + 4) / 4;  // float4s per candidate
+    const int per_c = G * kRecFloats<D> / 4;  // 16-byte vectors per candidate
     const float4_t *src = reinterpret_cast<const float4_t *>(deferred);
     for (int u = lane; u < p.C * per_c; u += kWave) {
       const int c = u / per_c;
       const size_t rec0 = (((size_t)dsplit * p.S + pp * p.C + c) * p.L + l) * p.Hq + h * G;
-      reinterpret_cast<float4_t *>(p.ws + rec0 * (D + 4))[u - c * per_c] = src[u];
+      reinterpret_cast<float4_t *>(p.ws + rec0 * kRecFloats<D>)[u - c * per_c] = src[u];
     }
   }
 }
@@ -743,7 +769,7 @@ __global__ __launch_bounds__(64) void attn_f32(AttnParams p, int nt_max) {
 // LDS of a context-kernel wave: the deferred records of RB * 16 rows.
 template <int D>
 size_t prefix_lds_bytes(int rb) {
-  return (size_t)rb * 16 * (D + 4) * sizeof(float);
+  return (size_t)rb * 16 * kRecFloats<D> * sizeof(float);
 }
 
 template <int D>
@@ -752,7 +778,7 @@ hipError_t launch_bf16(const AttnParams &p_in, hipStream_t stream) {
   if (p.P > 0) {
     // LDS for the suffix kernel's prefetched partials: whole 1 KiB blocks per
     // piece, at most 16 KiB per wave (8 waves per CU then use 128 of 160 KiB).
-    p.merge_blk = (p.G * (D + 4) * 4 + 1023) / 1024 * 256;
+    p.merge_blk = (p.G * kRecFloats<D> * 4 + 1023) / 1024 * 256;
     const int fit = 16384 / (p.merge_blk * 4);
     p.merge_pf = p.nsplit < fit ? p.nsplit : fit;
   }
@@ -839,7 +865,7 @@ void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int *n
 }
 
 size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit) {
-  return (size_t)nsplit * S * L * Hq * (D + 4) * sizeof(float);
+  return (size_t)nsplit * S * L * Hq * (D == 128 ? kRecFloats<128> : kRecFloats<64>) * sizeof(float);
 }
 
 hipError_t launch_decode_attn(const AttnParams &p, hipStream_t stream) {

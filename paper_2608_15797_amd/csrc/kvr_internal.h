@@ -26,7 +26,8 @@ struct AttnParams {
   // scoring (scores == nullptr: off)
   float *scores;
   int B, W, buffer;
-  // split-K partials for the prefix path: ws [nsplit][S][L][Hq][D+4] floats.
+  // split-K partials for the prefix path: ws [nsplit][S][L][Hq] records of
+  // 4 + D/2 float slots ((max, sum, -, -) then o / sum as D float16).
   // The context kernel's nwaves waves each take `span` consecutive keys of
   // the flattened (prefix, layer, KV head, key) space; a unit is covered by at
   // most nsplit of them, each leaving one partial record.

@@ -87,7 +87,8 @@ def test_prefix_workspace_size_matches_split_plan():
     c = _cache(kvr, S=128, L=28, Hkv=2, cap=512)
     p = kvr.c_prefix(16, 16, 16, 8192)
     n = kvr.lib.kvr_decode_attn_workspace_size(ctypes.byref(c), ctypes.byref(p), 12)
-    rec = 128 * 28 * 12 * (128 + 4) * 4
+    # One record per query row and split: (max, sum, -, -) float32 + 128 float16.
+    rec = 128 * 28 * 12 * (16 + 128 * 2)
     assert n % rec == 0 and n // rec >= 2
 
 
