@@ -344,7 +344,9 @@ def test_evict_topb_ties_and_gpu_scores_selection():
     (torch.bfloat16, 128, 16, 33, 130),    # 33 row blocks: the last pair is half empty
     (torch.bfloat16, 128, 1, 3, 40),       # fewer rows than one block
     (torch.bfloat16, 128, 7, 128, 300),    # a committed step's window on the 7B head shape
-    (torch.bfloat16, 128, 4, 8, 16384),    # largest cache: the accumulator fills 64 KB of LDS
+    (torch.bfloat16, 128, 4, 8, 12288),    # largest cache of the LDS-ring kernel: accumulator + ring = 64 KB
+    (torch.bfloat16, 64, 4, 8, 15000),     # beyond it at D = 64: the single-wave-stream kernel
+    (torch.bfloat16, 128, 4, 8, 16384),    # largest cache: the accumulator alone fills 64 KB of LDS
 ])
 def test_accumulate_scores(dt, D, G, nq, cap):
     """kvr_accumulate_scores equals the oracle's causal window re-computation,
