@@ -116,8 +116,9 @@ __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int
       const int i = c0 + e / row_units;
       if (i < p.B) {
         const int u = e % row_units;
-        reinterpret_cast<u32x4 *>(Kb + (size_t)i * row_bytes)[u] = kr[a];
-        reinterpret_cast<u32x4 *>(Vb + (size_t)i * row_bytes)[u] = vr[a];
+        // Non-temporal: the compacted rows are next read a decode step later.
+        __builtin_nontemporal_store(kr[a], reinterpret_cast<u32x4 *>(Kb + (size_t)i * row_bytes) + u);
+        __builtin_nontemporal_store(vr[a], reinterpret_cast<u32x4 *>(Vb + (size_t)i * row_bytes) + u);
       }
     }
     if (pos && tid < chunk_rows && c0 + tid < p.B) pos[c0 + tid] = pr;
