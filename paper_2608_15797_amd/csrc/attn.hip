@@ -124,7 +124,7 @@ __device__ __forceinline__ void load_chunk(KVChunk<D, TILES> &c, rsrc_t K, rsrc_
     const uint32_t base = (uint32_t)(c0 + t * 16 + r16) * ROW + g4 * 16;
 #pragma unroll
     for (int i = 0; i < Geo<D>::NLD; i++)
-      c.k[t][i] = __builtin_amdgcn_raw_buffer_load_b128(K, base + i * 64, 0, 0);
+      c.k[t][i] = __builtin_amdgcn_raw_buffer_load_b128(K, base + i * 64, 0, kStreamLoad);
   }
 #pragma unroll
   for (int t = 0; t < TILES; t++)
@@ -132,10 +132,10 @@ __device__ __forceinline__ void load_chunk(KVChunk<D, TILES> &c, rsrc_t K, rsrc_
     for (int cc = 0; cc < 4; cc++) {
       const uint32_t off = (uint32_t)(c0 + t * 16 + 4 * g4 + cc) * ROW + r16 * (Geo<D>::NB * 2);
       if constexpr (D == 128) {
-        const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(V, off, 0, 0);
+        const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(V, off, 0, kStreamLoad);
         c.v[t][cc][0] = x.x; c.v[t][cc][1] = x.y; c.v[t][cc][2] = x.z; c.v[t][cc][3] = x.w;
       } else {
-        const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(V, off, 0, 0);
+        const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(V, off, 0, kStreamLoad);
         c.v[t][cc][0] = x.x; c.v[t][cc][1] = x.y;
       }
     }

@@ -107,7 +107,7 @@ template <>
 struct Vec8<bf16_t> {
   u32x4 w;
   __device__ __forceinline__ void load(rsrc_t r, int v) {
-    w = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 16u, 0, 0);
+    w = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 16u, 0, kStreamLoad);
   }
   __device__ __forceinline__ void get(float (&y)[8]) const {
     y[0] = bf16_lo(w.x); y[1] = bf16_hi(w.x); y[2] = bf16_lo(w.y); y[3] = bf16_hi(w.y);
@@ -118,8 +118,8 @@ template <>
 struct Vec8<float> {
   u32x4 a, b;
   __device__ __forceinline__ void load(rsrc_t r, int v) {
-    a = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u, 0, 0);
-    b = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u + 16u, 0, 0);
+    a = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u, 0, kStreamLoad);
+    b = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u + 16u, 0, kStreamLoad);
   }
   __device__ __forceinline__ void get(float (&y)[8]) const {
     y[0] = __uint_as_float(a.x); y[1] = __uint_as_float(a.y); y[2] = __uint_as_float(a.z); y[3] = __uint_as_float(a.w);

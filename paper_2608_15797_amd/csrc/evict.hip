@@ -102,8 +102,8 @@ __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int
       if (i < p.B) {
         const int src = kept[i];
         const int u = e % row_units;
-        kr[a] = reinterpret_cast<const u32x4 *>(Kb + (size_t)src * row_bytes)[u];
-        vr[a] = reinterpret_cast<const u32x4 *>(Vb + (size_t)src * row_bytes)[u];
+        kr[a] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(Kb + (size_t)src * row_bytes) + u);
+        vr[a] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(Vb + (size_t)src * row_bytes) + u);
       }
     }
     if (pos && tid < chunk_rows && c0 + tid < p.B) pr = pos[kept[c0 + tid]];

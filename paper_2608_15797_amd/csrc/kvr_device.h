@@ -14,6 +14,10 @@ typedef float float2_t __attribute__((ext_vector_type(2)));
 constexpr int kWave = 64;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+// Cache-policy operand of the buffer loads of data that one launch reads once
+// (cache rows, logits rows): the nt (streaming) hint, so the lines do not
+// displace reused data in L2.
+constexpr int kStreamLoad = 2;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }

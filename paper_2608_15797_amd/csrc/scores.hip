@@ -336,7 +336,7 @@ __global__ __launch_bounds__(NW * 64) void window_scores_tiled(ScoreParams p) {
       const int row = RPI * I + lane / RU;
       const int u = (lane % RU) ^ (row % RU);
       const uint32_t off = ((uint32_t)(kt * kTK + row) * RU + (uint32_t)u) * 16u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_t *)(slot + I * 1024), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_t *)(slot + I * 1024), 16, off, 0, 0, kStreamLoad);
     }
 #endif
   };
