@@ -281,6 +281,8 @@ __global__ __launch_bounds__(256) void window_scores_bf16(ScoreParams p) {
 // operand reads (16 keys x one unit each) hit distinct banks. The kernel is
 // bound by its arithmetic (two exps per row and key): with NW = 8, KRB = 2
 // (4 waves per SIMD) measured fastest, ahead of fewer K passes at KRB = 4.
+// The key loads keep the default cache policy: the second pass finds the
+// head's keys in L2 (the streaming hint measured 2% slower).
 constexpr int kTK = 32;  // keys per LDS tile
 constexpr float kSlack = 8.0f;  // log2 units the first pass's reference may trail its maximum
 
@@ -336,7 +338,7 @@ __global__ __launch_bounds__(NW * 64) void window_scores_tiled(ScoreParams p) {
       const int row = RPI * I + lane / RU;
       const int u = (lane % RU) ^ (row % RU);
       const uint32_t off = ((uint32_t)(kt * kTK + row) * RU + (uint32_t)u) * 16u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_t *)(slot + I * 1024), 16, off, 0, 0, kStreamLoad);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_t *)(slot + I * 1024), 16, off, 0, 0, 0);
     }
 #endif
   };
