@@ -54,9 +54,8 @@ def step_bytes(wl, dec, i, moved_rows=None):
             out["evict"] = acc.evict_bytes(wl, n, moved_rows)
     if wl.helper:
         out["helper_attn"] = acc.helper_attn_bytes(wl, dec.hlen_host[i])
-    e = acc.esize(wl)
-    for w, ls in enumerate(wl.logits):
-        out["entropy%d" % w] = ls.R * ls.V * e + ls.R * 4
+    if wl.logits:
+        out["entropy"] = acc.entropy_bytes(wl)  # every logit set, one batched call
     return out
 
 

@@ -255,6 +255,45 @@ int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, i
 
 size_t kvr_logit_entropy_workspace_size(int32_t R, int32_t V);
 
+/* One set of logit rows for kvr_logit_entropy_batch; the fields mean what the
+ * arguments of kvr_logit_entropy of the same names mean. */
+typedef struct kvr_logit_set {
+    const void *logits;   /* [R][ld] of dtype */
+    int32_t dtype;
+    int32_t R, V;
+    int64_t ld;
+    float inv_temp;
+    float *H;             /* [R] float32 output */
+    const kvr_detector *det;  /* NULL or this set's own detector state */
+} kvr_logit_set;
+
+#define KVR_ENTROPY_MAX_SETS 4
+
+/*
+ * kvr_logit_entropy_batch -- kvr_logit_entropy over several sets of rows in
+ * one pass: the token entropies of every model that decodes in a step (the
+ * base and helper logits of Eq. (4), one launch for all candidates and both
+ * vocabularies, Sec. 3.1 batching). Each set keeps its own vocabulary size,
+ * row stride, temperature, output and detector.
+ *
+ *   sets      : nsets descriptors in host memory (read during the call only).
+ *   nsets     : 1 .. KVR_ENTROPY_MAX_SETS; every set has the same dtype, and
+ *               the total row count is at most 65535.
+ *   workspace : at least kvr_logit_entropy_batch_workspace_size(sets, nsets)
+ *               bytes, 16-byte aligned (no initialisation); may be NULL/0
+ *               when that size is 0.
+ * The H and detector arrays of different sets must not overlap.
+ * Errors: KVR_EINVAL (a set's arguments as for kvr_logit_entropy, nsets out
+ * of range, mixed dtypes, too many rows), KVR_EUNSUPPORTED (dtype),
+ * KVR_EWORKSPACE, KVR_EHIP. Nothing is enqueued on error.
+ */
+int kvr_logit_entropy_batch(const kvr_logit_set *sets, int32_t nsets, void *workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+
+/* Depends on the sets' dtype, R, V, ld and inv_temp only (their pointers
+ * are not read); 0 when those are invalid. */
+size_t kvr_logit_entropy_batch_workspace_size(const kvr_logit_set *sets, int32_t nsets);
+
 /*
  * kvr_logit_entropy_sample -- kvr_logit_entropy and the next token of every
  * row from the same single pass over the logits (Eq. (4) entropy and the

@@ -315,6 +315,68 @@ int kvr_logit_entropy(const void *logits, int32_t dtype, int32_t R, int32_t V, i
   return hip_status(kvr::launch_logit_entropy(p, stream), "kvr_logit_entropy launch");
 }
 
+}  // extern "C"
+
+namespace {
+
+// Validates a batch and fills b (all but the workspace pointers); *need gets
+// the workspace size. With shapes_only, the sets' pointers are not checked
+// (the workspace size depends on the shapes alone).
+int entropy_batch(const kvr_logit_set *sets, int32_t nsets, kvr::EntropyBatch *b, size_t *need,
+                  bool shapes_only = false) {
+  if (!sets) return fail(KVR_EINVAL, "sets is required");
+  if (nsets < 1 || nsets > kvr::kEntropyMaxSets)
+    return fail(KVR_EINVAL, "nsets=%d outside 1..%d", nsets, kvr::kEntropyMaxSets);
+  *b = kvr::EntropyBatch{};
+  b->nsets = nsets;
+  long rows = 0;
+  int vmin = 0;
+  for (int k = 0; k < nsets; k++) {
+    const kvr_logit_set &s = sets[k];
+    const void *any = reinterpret_cast<const void *>(16);
+    int st = shapes_only ? entropy_params(any, s.dtype, s.R, s.V, s.ld, s.inv_temp, (float *)any, nullptr, &b->set[k])
+                         : entropy_params(s.logits, s.dtype, s.R, s.V, s.ld, s.inv_temp, s.H, s.det, &b->set[k]);
+    if (st) return st;
+    if (s.dtype != sets[0].dtype) return fail(KVR_EINVAL, "set %d dtype %d differs from set 0's %d", k, s.dtype, sets[0].dtype);
+    b->row0[k] = (int)rows;
+    rows += s.R;
+    if (rows > 65535) return fail(KVR_EINVAL, "%ld rows in the batch exceeds 65535", rows);
+    vmin = k == 0 || s.V < vmin ? s.V : vmin;
+  }
+  b->row0[nsets] = (int)rows;
+  const int splits = kvr::entropy_splits((int)rows, vmin);
+  for (int k = 0; k < nsets; k++) b->set[k].splits = splits;
+  *need = splits == 1 ? 0 : (size_t)rows * splits * 4 * sizeof(float);
+  return KVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t kvr_logit_entropy_batch_workspace_size(const kvr_logit_set *sets, int32_t nsets) {
+  kvr::EntropyBatch b;
+  size_t need = 0;
+  if (entropy_batch(sets, nsets, &b, &need, true)) return 0;
+  return need;
+}
+
+int kvr_logit_entropy_batch(const kvr_logit_set *sets, int32_t nsets, void *workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  kvr::EntropyBatch b;
+  size_t need = 0;
+  int st = entropy_batch(sets, nsets, &b, &need);
+  if (st) return st;
+  if (need) {
+    if (!workspace || workspace_bytes < need)
+      return fail(KVR_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+    if (!aligned16(workspace)) return fail(KVR_EINVAL, "workspace not 16-byte aligned");
+    for (int k = 0; k < nsets; k++)
+      b.set[k].ws = static_cast<char *>(workspace) + (size_t)b.row0[k] * b.set[k].splits * 4 * sizeof(float);
+  }
+  return hip_status(kvr::launch_logit_entropy_batch(b, stream), "kvr_logit_entropy_batch launch");
+}
+
 size_t kvr_logit_entropy_sample_workspace_size(int32_t R, int32_t V, int32_t top_k) {
   if (R <= 0 || V <= 0 || top_k < 1 || top_k > kvr::kTopKMax) return 0;
   return kvr::sample_workspace_bytes(R, V, top_k);

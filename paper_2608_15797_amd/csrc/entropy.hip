@@ -45,6 +45,7 @@ namespace kvr {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kRoundVecs = 10 * kThreads;  // 8-logit vectors per workgroup per round (entropy alone)
 constexpr float kNegInf = -__builtin_huge_valf();
 
 struct Tri {
@@ -373,15 +374,27 @@ __device__ __forceinline__ int gather_select(const uint64_t *cand, const int (&o
   return wave_store_ge<NPL>(out, v, thr, lane);
 }
 
+// The set of a batch that holds global row g (uniform per workgroup).
+__device__ __forceinline__ int batch_set(const EntropyBatch &b, int g) {
+  int k = 0;
+#pragma unroll
+  for (int i = 1; i < kEntropyMaxSets; i++)
+    if (i < b.nsets && g >= b.row0[i]) k = i;
+  return k;
+}
+
+// One workgroup per (split, global row of the batch).
 // VEC = true: 16-byte loads of 8 elements (row starts 16-byte aligned).
 // SAMPLE = true: also collect the split's top_k candidates (always writes
 // the split's partials, even unsplit rows, for the sampling merge).
 template <typename T, bool VEC, bool SAMPLE>
-__global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
+__global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
   __shared__ Tri part[kThreads / kWave];
   __shared__ uint64_t cand[SAMPLE ? (kThreads / kWave) * kCandCap : 1];
   __shared__ int cand_n[kThreads / kWave];
-  const int row = blockIdx.y;
+  const int bset = batch_set(b, blockIdx.y);
+  const EntropyParams &p = b.set[bset];
+  const int row = blockIdx.y - b.row0[bset];
   const int split = blockIdx.x;
   const int splits = gridDim.x;
   const int tid = threadIdx.x;
@@ -398,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyParams p) {
     // round overlaps its later loads. Entropy alone: 10, so that a split of
     // the 7B / 1.5B vocabularies over 8 workgroups per row is one round. With
     // the sampler: 8, whose lower register count keeps 4 waves per SIMD.
-    constexpr int U = SAMPLE ? 8 : 10;
+    constexpr int U = SAMPLE ? 8 : kRoundVecs / kThreads;
     const int nvec = p.V / 8;
     const int per = (nvec + splits - 1) / splits;
     const int v0 = split * per;
@@ -547,9 +560,12 @@ __device__ __forceinline__ Tri wave_merge_splits(const EntropyParams &p, int row
   return acc;
 }
 
-// Per-row merge of the split partials, then the detector; one wave per row.
-__global__ __launch_bounds__(kWave) void entropy_merge(EntropyParams p) {
-  const int row = blockIdx.x;
+// Per-row merge of the split partials, then the detector; one wave per
+// global row of the batch.
+__global__ __launch_bounds__(kWave) void entropy_merge(EntropyBatch b) {
+  const int bset = batch_set(b, blockIdx.x);
+  const EntropyParams &p = b.set[bset];
+  const int row = blockIdx.x - b.row0[bset];
   const int lane = threadIdx.x;
   const float H = finish_entropy(wave_merge_splits(p, row, lane));
   if (lane == 0) p.H[row] = H;
@@ -627,11 +643,15 @@ __global__ __launch_bounds__(kWave) void sample_merge(EntropyParams p) {
 
 int entropy_splits(int R, int V) {
   // Enough workgroups to cover the chip (~1024), but at least 1024 vectors of
-  // 8 logits per workgroup.
+  // 8 logits per workgroup; and, when the rows alone fill the chip, still no
+  // more than one round of the vector loop per workgroup (measured: 256 rows
+  // of 152k logits in 8 splits, 2048 workgroups, beat 4 splits by 6%).
   const long nvec = V / 8;
   long s = (1024 + R - 1) / R;
   const long maxs = nvec / 1024 > 0 ? nvec / 1024 : 1;
   if (s > maxs) s = maxs;
+  const long one_round = (nvec + kRoundVecs - 1) / kRoundVecs;
+  if (s < one_round) s = one_round;
   if (s < 1) s = 1;
   if (s > 1024) s = 1024;
   return (int)s;
@@ -655,35 +675,52 @@ size_t sample_workspace_bytes(int R, int V, int top_k) {
 }
 
 template <typename T, bool VEC>
-static void launch_split(const EntropyParams &p, dim3 grid, hipStream_t stream) {
-  if (p.top_k > 0) hipLaunchKernelGGL((entropy_kernel<T, VEC, true>), grid, dim3(kThreads), 0, stream, p);
-  else hipLaunchKernelGGL((entropy_kernel<T, VEC, false>), grid, dim3(kThreads), 0, stream, p);
+static void launch_split(const EntropyBatch &b, bool sample, dim3 grid, hipStream_t stream) {
+  if (sample) hipLaunchKernelGGL((entropy_kernel<T, VEC, true>), grid, dim3(kThreads), 0, stream, b);
+  else hipLaunchKernelGGL((entropy_kernel<T, VEC, false>), grid, dim3(kThreads), 0, stream, b);
+}
+
+// The split pass over every row of the batch (one launch), with 16-byte
+// loads when every set's rows start 16-byte aligned.
+static hipError_t launch_partials(const EntropyBatch &b, bool sample, hipStream_t stream) {
+  const EntropyParams &p0 = b.set[0];
+  const size_t esz = p0.dtype == 0 ? 4 : 2;
+  bool vec = true;
+  for (int k = 0; k < b.nsets; k++)
+    vec = vec && ((uintptr_t)b.set[k].logits % 16 == 0) && ((size_t)b.set[k].ld * esz % 16 == 0);
+  const dim3 grid(p0.splits, b.row0[b.nsets]);
+  if (p0.dtype == 0) {
+    if (vec) launch_split<float, true>(b, sample, grid, stream);
+    else launch_split<float, false>(b, sample, grid, stream);
+  } else {
+    if (vec) launch_split<bf16_t, true>(b, sample, grid, stream);
+    else launch_split<bf16_t, false>(b, sample, grid, stream);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_logit_entropy_batch(const EntropyBatch &b, hipStream_t stream) {
+  hipError_t e = launch_partials(b, false, stream);
+  if (e != hipSuccess || b.set[0].splits == 1) return e;
+  hipLaunchKernelGGL(entropy_merge, dim3(b.row0[b.nsets]), dim3(kWave), 0, stream, b);
+  return hipGetLastError();
 }
 
 hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream) {
-  const dim3 grid(p.splits, p.R);
-  const size_t esz = p.dtype == 0 ? 4 : 2;
-  const bool vec = ((uintptr_t)p.logits % 16 == 0) && ((size_t)p.ld * esz % 16 == 0);
-  if (p.dtype == 0) {
-    if (vec) launch_split<float, true>(p, grid, stream);
-    else launch_split<float, false>(p, grid, stream);
-  } else {
-    if (vec) launch_split<bf16_t, true>(p, grid, stream);
-    else launch_split<bf16_t, false>(p, grid, stream);
-  }
-  hipError_t e = hipGetLastError();
+  EntropyBatch b{};
+  b.set[0] = p;
+  b.row0[0] = 0;
+  b.row0[1] = p.R;
+  b.nsets = 1;
+  if (p.top_k <= 0) return launch_logit_entropy_batch(b, stream);
+  hipError_t e = launch_partials(b, true, stream);
   if (e != hipSuccess) return e;
-  if (p.top_k > 0) {
-    const int E = p.splits * p.top_k;
-    if (E <= 64) hipLaunchKernelGGL(sample_merge<1>, dim3(p.R), dim3(kWave), 0, stream, p);
-    else if (E <= 128) hipLaunchKernelGGL(sample_merge<2>, dim3(p.R), dim3(kWave), 0, stream, p);
-    else if (E <= 256) hipLaunchKernelGGL(sample_merge<4>, dim3(p.R), dim3(kWave), 0, stream, p);
-    else if (E <= 512) hipLaunchKernelGGL(sample_merge<8>, dim3(p.R), dim3(kWave), 0, stream, p);
-    else hipLaunchKernelGGL(sample_merge<16>, dim3(p.R), dim3(kWave), 0, stream, p);
-    return hipGetLastError();
-  }
-  if (p.splits == 1) return e;
-  hipLaunchKernelGGL(entropy_merge, dim3(p.R), dim3(kWave), 0, stream, p);
+  const int E = p.splits * p.top_k;
+  if (E <= 64) hipLaunchKernelGGL(sample_merge<1>, dim3(p.R), dim3(kWave), 0, stream, p);
+  else if (E <= 128) hipLaunchKernelGGL(sample_merge<2>, dim3(p.R), dim3(kWave), 0, stream, p);
+  else if (E <= 256) hipLaunchKernelGGL(sample_merge<4>, dim3(p.R), dim3(kWave), 0, stream, p);
+  else if (E <= 512) hipLaunchKernelGGL(sample_merge<8>, dim3(p.R), dim3(kWave), 0, stream, p);
+  else hipLaunchKernelGGL(sample_merge<16>, dim3(p.R), dim3(kWave), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -103,12 +103,22 @@ struct EntropyParams {
   uint64_t seed, step;
   int32_t *tokens;
 };
+// Several sets of rows in one launch: global row g belongs to the set k with
+// row0[k] <= g < row0[k + 1]. Every set has the same dtype and split count,
+// and its ws points at its own R * splits partial records.
+constexpr int kEntropyMaxSets = 4;
+struct EntropyBatch {
+  EntropyParams set[kEntropyMaxSets];
+  int row0[kEntropyMaxSets + 1];
+  int nsets;
+};
 int entropy_splits(int R, int V);
 size_t entropy_workspace_bytes(int R, int V);
 int sample_splits(int R, int V, int top_k);
 size_t sample_workspace_bytes(int R, int V, int top_k);
 constexpr int kTopKMax = 64;
 hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream);
+hipError_t launch_logit_entropy_batch(const EntropyBatch &b, hipStream_t stream);
 
 struct ForkParams {
   const void *sk, *sv;

@@ -26,7 +26,7 @@ EXPORTS = ("kvr_strerror", "kvr_last_error", "kvr_decode_attn", "kvr_decode_attn
            "kvr_accumulate_scores", "kvr_evict_topb", "kvr_logit_entropy",
            "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append",
            "kvr_logit_entropy_sample", "kvr_logit_entropy_sample_workspace_size",
-           "kvr_redundancy_scores")
+           "kvr_redundancy_scores", "kvr_logit_entropy_batch", "kvr_logit_entropy_batch_workspace_size")
 
 
 class KvrError(RuntimeError):
@@ -53,6 +53,12 @@ class c_policy(ctypes.Structure):
 class c_detector(ctypes.Structure):
     _fields_ = [("hist", ctypes.c_void_p), ("cnt", ctypes.c_void_p), ("flag", ctypes.c_void_p),
                 ("window", ctypes.c_int32), ("guard", ctypes.c_int32), ("tau", ctypes.c_float)]
+
+
+class c_logit_set(ctypes.Structure):
+    _fields_ = [("logits", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("R", ctypes.c_int32),
+                ("V", ctypes.c_int32), ("ld", ctypes.c_int64), ("inv_temp", ctypes.c_float),
+                ("H", ctypes.c_void_p), ("det", ctypes.POINTER(c_detector))]
 
 
 class c_sampler(ctypes.Structure):
@@ -85,6 +91,10 @@ def _load():
     lib.kvr_logit_entropy.restype = ctypes.c_int
     lib.kvr_logit_entropy_workspace_size.argtypes = [i32, i32]
     lib.kvr_logit_entropy_workspace_size.restype = sz
+    lib.kvr_logit_entropy_batch.argtypes = [P(c_logit_set), i32, vp, sz, vp]
+    lib.kvr_logit_entropy_batch.restype = ctypes.c_int
+    lib.kvr_logit_entropy_batch_workspace_size.argtypes = [P(c_logit_set), i32]
+    lib.kvr_logit_entropy_batch_workspace_size.restype = sz
     lib.kvr_logit_entropy_sample.argtypes = [vp, i32, i32, i32, i64, f32, vp, P(c_detector),
                                              P(c_sampler), vp, vp, sz, vp]
     lib.kvr_logit_entropy_sample.restype = ctypes.c_int
@@ -263,6 +273,47 @@ def logit_entropy(logits: torch.Tensor, H: torch.Tensor, V: Optional[int] = None
                                0 if workspace is None else workspace.numel() * workspace.element_size(),
                                _stream(stream))
     _check(rc, "kvr_logit_entropy")
+
+
+@dataclass
+class LogitSet:
+    """One set of logit rows of kvr_logit_entropy_batch: logits[R][ld] (first
+    V columns), H[R] output, optional detector."""
+    logits: torch.Tensor
+    H: torch.Tensor
+    V: Optional[int] = None
+    inv_temp: float = 1.0
+    detector: Optional[Detector] = None
+
+
+def _logit_sets(sets) -> ctypes.Array:
+    arr = (c_logit_set * len(sets))()
+    for k, s in enumerate(sets):
+        lg = s.logits
+        assert lg.dim() == 2 and lg.stride(1) == 1
+        det = ctypes.pointer(s.detector.c()) if s.detector is not None else None
+        arr[k] = c_logit_set(_ptr(lg), dtype_code(lg.dtype), lg.shape[0],
+                             lg.shape[1] if s.V is None else s.V, lg.stride(0), float(s.inv_temp),
+                             _ptr(s.H), det)
+    return arr
+
+
+def logit_entropy_batch_workspace_size(shapes, dtype=torch.bfloat16) -> int:
+    """Workspace bytes of kvr_logit_entropy_batch for sets of (R, V) rows of
+    `dtype` (the size depends on the shapes only)."""
+    arr = (c_logit_set * len(shapes))()
+    for k, (R, V) in enumerate(shapes):
+        arr[k] = c_logit_set(None, dtype_code(dtype), R, V, V, 1.0, None, None)
+    return int(lib.kvr_logit_entropy_batch_workspace_size(arr, len(shapes)))
+
+
+def logit_entropy_batch(sets, workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """kvr_logit_entropy_batch over a list of LogitSet (one launch for all rows)."""
+    arr = _logit_sets(sets)
+    rc = lib.kvr_logit_entropy_batch(arr, len(sets), _ptr(workspace),
+                                     0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                     _stream(stream))
+    _check(rc, "kvr_logit_entropy_batch")
 
 
 def fork(src: Cache, dst: Cache, src_index: torch.Tensor, len_: torch.Tensor,

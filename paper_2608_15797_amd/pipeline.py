@@ -7,8 +7,9 @@ helper candidates of every problem decode together) is:
   2. base:   kvr_evict_topb when the live length exceeds B + buffer;
   3. helper: kvr_decode_attn over the shared or private full context plus the
              candidate's own suffix (Sec. 3.1);
-  4. kvr_logit_entropy over every logit row, with the moving-average detector
-             on the base rows (Eq. (4); only base candidates are screened).
+  4. kvr_logit_entropy_batch over the logit rows of both models in one
+             launch, with the moving-average detector on the base rows
+             (Eq. (4); only base candidates are screened).
 
 All candidates advance in lockstep, so every live length is known on the host
 in advance: the driver precomputes per-token length tables on the device
@@ -114,6 +115,10 @@ class Decoder:
         # Only base candidates are screened (Sec. 3.2); helper rows get entropy only.
         self.detector = kvr.Detector.zeros(wl.logits[0].R, win, guard, tau, dev) \
             if (wl.logits and wl.base) else None
+        # Workspace of the batched entropy call over every logit set.
+        if wl.logits:
+            n = kvr.logit_entropy_batch_workspace_size([(ls.R, ls.V) for ls in wl.logits], self.dt)
+            self.ews_batch = torch.zeros(max(n, 16) // 4 + 4, dtype=torch.float32, device=dev)
 
         # Input pool.
         self.per_token = per_token_inputs
@@ -186,11 +191,14 @@ class Decoder:
                             stream=stream)
 
     def entropy(self, si: StepInputs, stream=None, timers=None) -> None:
-        for w, lg in enumerate(si.logits):
-            with _timer(timers, "entropy%d" % w, stream):
-                kvr.logit_entropy(lg, self.H[w], V=self.wl.logits[w].V,
-                                  detector=self.detector if w == 0 else None,
-                                  workspace=self.ews[w], stream=stream)
+        """Entropies of every logit set of the step in one batched call."""
+        if not si.logits:
+            return
+        sets = [kvr.LogitSet(lg, self.H[w], self.wl.logits[w].V,
+                             detector=self.detector if w == 0 else None)
+                for w, lg in enumerate(si.logits)]
+        with _timer(timers, "entropy", stream):
+            kvr.logit_entropy_batch(sets, workspace=self.ews_batch, stream=stream)
 
     def prompt(self, stream=None) -> None:
         for t in range(self.T_prompt):

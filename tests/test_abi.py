@@ -82,6 +82,38 @@ def test_entropy_rejects_bad_arguments_on_host():
         assert "inv_temp" in kvr.lib.kvr_last_error().decode()
 
 
+def test_entropy_batch_rejects_bad_arguments_on_host():
+    from paper_2608_15797_amd import kvr
+
+    def sets(*specs):
+        arr = (kvr.c_logit_set * len(specs))()
+        for k, (dtype, R, V, ld, it) in enumerate(specs):
+            arr[k] = kvr.c_logit_set(16, dtype, R, V, ld, it, 16 + 4096 * k, None)
+        return arr
+
+    f, ws = kvr.lib.kvr_logit_entropy_batch, kvr.lib.kvr_logit_entropy_batch_workspace_size
+    two = sets((1, 128, 152064, 152064, 1.0), (1, 128, 151936, 151936, 1.0))
+    # Both vocabularies over one split plan: 256 rows x 8 splits of 16-byte partials.
+    assert ws(two, 2) == 256 * 8 * 16
+    assert f(two, 2, None, 0, None) == -4
+    assert f(two, 2, 16, 256 * 8 * 16 - 1, None) == -4
+    assert f(None, 2, None, 0, None) == -1
+    for n in (0, 5):
+        assert f(two, n, None, 0, None) == -1 and "nsets" in kvr.lib.kvr_last_error().decode()
+    # The size query reads shapes only.
+    assert kvr.logit_entropy_batch_workspace_size([(128, 152064), (128, 151936)]) == 256 * 8 * 16
+    assert kvr.logit_entropy_batch_workspace_size([(3, 10)]) == 0
+    mixed = sets((1, 4, 10, 10, 1.0), (0, 4, 10, 10, 1.0))
+    assert f(mixed, 2, None, 0, None) == -1 and "dtype" in kvr.lib.kvr_last_error().decode()
+    assert ws(mixed, 2) == 0
+    many = sets((1, 40000, 10, 10, 1.0), (1, 30000, 10, 10, 1.0))
+    assert f(many, 2, None, 0, None) == -1 and "rows" in kvr.lib.kvr_last_error().decode()
+    # Each set is checked as kvr_logit_entropy checks its arguments.
+    assert f(sets((1, 4, 10, 10, 1.0), (1, 4, 10, 5, 1.0)), 2, None, 0, None) == -1
+    assert f(sets((1, 4, 10, 10, 1.0), (1, 4, 10, 10, float("nan"))), 2, None, 0, None) == -1
+    assert f(sets((3, 4, 10, 10, 1.0)), 1, None, 0, None) == -2
+
+
 def test_prefix_workspace_size_matches_split_plan():
     from paper_2608_15797_amd import kvr
     c = _cache(kvr, S=128, L=28, Hkv=2, cap=512)

@@ -423,6 +423,62 @@ def test_logit_entropy(case):
     assert np.abs(H.cpu().double().numpy() - ref).max() <= 1e-4
 
 
+ENT_BATCH_CASES = [
+    # per set: R, V, ld, std, inv_temp, with detector
+    [(128, 152064, 152064, 3.0, 1.0, True), (128, 151936, 151936, 1.0, 1.25, False)],
+    [(1, 1000, 1000, 1.0, 1.0, False), (64, 152064, 152064, 0.1, 1.0, True),
+     (5, 2048, 2048, 2.0, 0.8, True), (300, 8000, 8000, 3.0, 1.0, False)],
+    [(3, 7, 9, 2.0, 1.0, False), (1, 1, 1, 1.0, 1.0, False), (4, 50000, 50003, 5.0, 1.0, True)],
+    [(32, 152064, 152064, 3.0, 1.0, True)],
+]
+
+
+@pytest.mark.parametrize("ci", range(len(ENT_BATCH_CASES)))
+@pytest.mark.parametrize("dt", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+def test_logit_entropy_batch(ci, dt):
+    """One launch over several sets of rows (different vocabularies, strides,
+    temperatures and detectors): every set's entropies match the oracle, and
+    each detector holds exactly its own set's history."""
+    k = kvr()
+    specs = ENT_BATCH_CASES[ci]
+    g = torch.Generator().manual_seed(71 + ci)
+    sets, hosts, odets = [], [], []
+    for j, (R, V, ld, std, it, with_det) in enumerate(specs):
+        x = torch.full((R, ld), 1e3)  # padding must be ignored
+        x[:, :V] = torch.randn((R, V), generator=g) * std
+        if V > 20:
+            x[0, 3:9] = float("-inf")
+            x[-1, :5] += 10.0
+        xd = x.to(dt)
+        det = k.Detector.zeros(R, window=12, guard=3, tau=5.0, device=DEV) if with_det else None
+        sets.append(k.LogitSet(xd.to(DEV), torch.full((R,), float("nan"), device=DEV), V, it, det))
+        hosts.append(xd)
+        odets.append(oracle.Detector(R, window=12, guard=3, tau=5.0) if with_det else None)
+    need = k.logit_entropy_batch_workspace_size([(s[0], s[1]) for s in specs], dt)
+    ws = torch.zeros(max(need, 16) // 4, device=DEV)
+    say("case", ci, "sets", [(s[0], s[1]) for s in specs], "workspace", need)
+    for rep in range(4):  # the workspace needs no reset between calls
+        for s in sets:
+            s.H.fill_(float("nan"))
+        k.logit_entropy_batch(sets, workspace=ws)
+        torch.cuda.synchronize()
+        for j, (s, xh, od) in enumerate(zip(sets, hosts, odets)):
+            ref = oracle.entropy(host(xh), V=specs[j][1], inv_temp=specs[j][4])
+            got = s.H.cpu().double().numpy()
+            d = np.abs(got - ref).max()
+            say("rep", rep, "set", j, "max abs err", d)
+            assert d <= 1e-4
+            if od is not None:
+                fref = od.step(ref)
+                assert s.detector.cnt.cpu().numpy().tolist() == [rep + 1] * specs[j][0]
+                f = s.detector.flag.cpu().numpy()
+                for r in range(specs[j][0]):
+                    mean = od.hist[r, :min(int(od.cnt[r]), 12)].mean()
+                    if od.cnt[r] >= 3 and abs(mean - 5.0) < 1e-4:
+                        continue
+                    assert f[r] == fref[r], (rep, j, r)
+
+
 def test_entropy_closed_forms_on_gpu():
     k = kvr()
     V = 152064
