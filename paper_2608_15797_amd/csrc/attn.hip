@@ -173,6 +173,26 @@ __device__ __forceinline__ void chunk_logits(const KVChunk<D, TILES> &c, const s
 // Loads past the resource's range return zero without touching memory, so
 // the ring is refilled unconditionally; pre() runs once the first loads are
 // in flight, then proc(chunk, c0) sees each real chunk.
+// stream_chunks with the ring supplied by the caller, whose buf[0] already
+// holds (or is loading) the chunk at k0.
+template <int D, int TILES, int DEPTH, typename Pre, typename Proc>
+__device__ __forceinline__ void stream_chunks_from(KVChunk<D, TILES> (&buf)[DEPTH], rsrc_t K, rsrc_t V, int k0,
+                                                   int k1, int r16, int g4, Pre pre, Proc proc) {
+  constexpr int stride = 16 * TILES;
+#pragma unroll
+  for (int s = 1; s < DEPTH - 1; s++) load_chunk<D, TILES>(buf[s], K, V, k0 + s * stride, r16, g4);
+  pre();
+  for (int c0 = k0; c0 < k1; c0 += DEPTH * stride) {
+#pragma unroll
+    for (int j = 0; j < DEPTH; j++) {
+      const int cj = c0 + j * stride;
+      if (cj >= k1) break;
+      load_chunk<D, TILES>(buf[(j + DEPTH - 1) % DEPTH], K, V, cj + (DEPTH - 1) * stride, r16, g4);
+      proc(buf[j], cj);
+    }
+  }
+}
+
 template <int D, int TILES, int DEPTH, typename Pre, typename Proc>
 __device__ __forceinline__ void stream_chunks(rsrc_t K, rsrc_t V, int k0, int k1, int r16, int g4,
                                               Pre pre, Proc proc) {
@@ -302,7 +322,7 @@ __device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st, f
 // next chunk's loads are in flight while the current one is computed; the
 // appended token (slot n-1) is a final one-key tile read from k_new/v_new.
 template <int D, bool MERGE, int TILES, int DEPTH>
-__global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void attn_cache_bf16(AttnParams p) {
   constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
   constexpr uint32_t ROW = D * 2;
@@ -317,14 +337,36 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   const int r16 = lane & 15;
   const int g4 = lane >> 4;
   const int G = p.G;
-
-  int n = p.len[s];
-  n = n < 0 ? 0 : (n > p.cap ? p.cap : n);
+  const int qh0 = h * G;
+  const size_t qrow0 = ((size_t)s * p.L + l) * p.Hq + qh0;
   const size_t ubase = (size_t)unit * p.cap * D;
   bf16_t *Kc = static_cast<bf16_t *>(p.k) + ubase;
   bf16_t *Vc = static_cast<bf16_t *>(p.v) + ubase;
   const bf16_t *kn = p.k_new ? static_cast<const bf16_t *>(p.k_new) + (size_t)unit * D : nullptr;
   const bf16_t *vn = p.v_new ? static_cast<const bf16_t *>(p.v_new) + (size_t)unit * D : nullptr;
+
+  // The loads that do not depend on the live length are issued before it is
+  // read: the query rows and the new token's one-key tile and, for an evicted
+  // cache (whose live length is at least B once the prompt is in), the first
+  // cache chunk, read over the first min(cap, CH) slots. A unit then exposes
+  // one memory round trip instead of two. Slots of that chunk at or past the
+  // end of the live cache hold stale rows: their keys are masked to -inf like
+  // any tail chunk's, and their value rows are zeroed before use (a stale row
+  // may hold NaN, and 0 * NaN would reach the output). A suffix cache starts
+  // empty after every committed step, so there the chunk waits for the length
+  // and reads no stale rows.
+  short4_t qop[NB];
+  load_qop<D>(r16 < G ? static_cast<const bf16_t *>(p.q) + (qrow0 + r16) * D : nullptr, g4, qop);
+  KVChunk<D, 1> cn;
+  if (kn) load_chunk<D, 1>(cn, make_rsrc(kn, ROW), make_rsrc(vn, ROW), 0, r16, g4);
+  KVChunk<D, TILES> ring[DEPTH];
+  if constexpr (!MERGE) {
+    const uint32_t first = (uint32_t)(p.cap < CH ? p.cap : CH) * ROW;
+    load_chunk<D, TILES>(ring[0], make_rsrc(Kc, first), make_rsrc(Vc, first), 0, r16, g4);
+  }
+
+  int n = p.len[s];
+  n = n < 0 ? 0 : (n > p.cap ? p.cap : n);
   const bool append = kn != nullptr && n >= 1;
   // The new token goes to slot n-1. Its K and V rows are loaded once, as the
   // one-key tile below, and written to the cache from those registers once
@@ -334,7 +376,6 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
   const int32_t npos = put_pos ? p.new_pos[s] : 0;
   const int ncache = append ? n - 1 : n;
 
-  const int qh0 = h * G;
   // Merge: the partial records of this wave's rows, piece k at stride
   // S*L*Hq records, G contiguous records each. The first merge_pf pieces
   // are copied into LDS now (buffer-to-LDS loads, 1 KiB per instruction) so
@@ -357,9 +398,6 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
     }
 #endif
   }
-  const size_t qrow0 = ((size_t)s * p.L + l) * p.Hq + qh0;
-  short4_t qop[NB];
-  load_qop<D>(r16 < G ? static_cast<const bf16_t *>(p.q) + (qrow0 + r16) * D : nullptr, g4, qop);
 
   // Observation-window step of this sequence?
   const int wstart = p.B + p.buffer + 2 - p.W;
@@ -376,7 +414,17 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
 
   const rsrc_t Kr = make_rsrc(Kc, (uint32_t)ncache * ROW);
   const rsrc_t Vr = make_rsrc(Vc, (uint32_t)ncache * ROW);
-  auto process = [&](const KVChunk<D, TILES> &c, int c0, int nlim) {
+  auto process = [&](KVChunk<D, TILES> &c, int c0, int nlim) {
+    if (!MERGE && c0 == 0 && nlim < CH) {
+      // The first chunk was read before the live length was known.
+#pragma unroll
+      for (int t = 0; t < TILES; t++)
+#pragma unroll
+        for (int cc = 0; cc < 4; cc++)
+          if (t * 16 + 4 * g4 + cc >= nlim)
+#pragma unroll
+            for (int w = 0; w < Geo<D>::VW; w++) c.v[t][cc][w] = 0u;
+    }
     float x[TILES][4];
     chunk_logits<D, TILES>(c, qop, x, c0, nlim, g4, sl2, c0 + CH > nlim);
     if (win && r16 < G) {
@@ -388,12 +436,9 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
     softmax_pv<D, TILES>(x, st, o, c.v, g4);
   };
 
-  // Every load a unit needs is issued up front so that only one memory round
-  // trip is exposed per unit: the new token's one-key tile (processed first;
-  // key order does not matter to the online softmax), the first cache chunk,
-  // and, in window steps that accumulate, the stored scores.
-  KVChunk<D, 1> cn;
-  if (append) load_chunk<D, 1>(cn, make_rsrc(kn, ROW), make_rsrc(vn, ROW), 0, r16, g4);
+  // The stored scores of window steps that accumulate are prefetched now,
+  // behind the loads issued above; the new token's tile is processed first
+  // (key order does not matter to the online softmax).
   constexpr int PRE = 5;  // stored scores prefetched per lane (slots < 320)
   const bool accumulate = win && n != wstart;
   float old[PRE];
@@ -429,8 +474,9 @@ __global__ __launch_bounds__(64) void attn_cache_bf16(AttnParams p) {
       softmax_pv<D, 1>(x, st, o, cn.v, g4);
     }
   };
-  stream_chunks<D, TILES, DEPTH>(Kr, Vr, 0, ncache, r16, g4, new_token,
-                                 [&](const KVChunk<D, TILES> &c, int c0) { process(c, c0, ncache); });
+  if constexpr (MERGE) load_chunk<D, TILES>(ring[0], Kr, Vr, 0, r16, g4);
+  stream_chunks_from<D, TILES, DEPTH>(ring, Kr, Vr, 0, ncache, r16, g4, new_token,
+                                      [&](KVChunk<D, TILES> &c, int c0) { process(c, c0, ncache); });
   if (append && win && r16 < G && g4 == 0) xs[r16 * ldx + n - 1] = xnew;
 
   float z = st.zl;

@@ -50,6 +50,8 @@ BASE_CASES = [
     (3, 2, 2, 6, 64, 40, 8, 30, torch.bfloat16),
     (2, 1, 1, 16, 128, 20, 5, 7, torch.bfloat16),
     (2, 2, 3, 1, 128, 20, 5, 7, torch.bfloat16),
+    # Cache shorter than one 32-key chunk, D = 64, with n = 1.
+    (5, 1, 2, 4, 64, 12, 4, 6, torch.bfloat16),
     # Largest scored cache at G = 16: the window logits fill 61.6 KB of LDS (limit 64 KB).
     (2, 1, 1, 16, 128, 704, 64, 255, torch.bfloat16),
 ]
