@@ -233,6 +233,16 @@ def traffic_for(name, call):
     return rec["bytes_per_call"]
 
 
+def attach_traffic(name, calls):
+    """Add the measured HBM bytes per call (and their ratio to the
+    algorithmic bytes) to every call that has a current traffic record."""
+    for call, c in calls.items():
+        t = traffic_for(name, call)
+        if t is not None:
+            c["measured_bytes_per_call"] = int(t)
+            c["measured_over_alg"] = round(t / c["bytes_per_call"], 4)
+
+
 def cpu_baseline(dec, wl, min_s=10.0):
     """The fp64 oracle timed on this host, on a bounded sample of the same
     workload: one problem's share of a decode step (its candidates' base
@@ -326,6 +336,7 @@ def main():
     res, dec, wl = run_workload(args.workload, args.steps, args.warmup, not args.no_instrument)
     steps = res["steps"]
     calls = res["calls"]
+    attach_traffic(args.workload, calls)
     roof = None
     if calls:
         dom = max(calls, key=lambda k: calls[k]["bytes_per_call"] * calls[k]["launches"])
@@ -347,6 +358,7 @@ def main():
     extra = {}
     for name in [x for x in args.extra.split(",") if x and x != args.workload]:
         r, d, _ = run_workload(name, 0, args.warmup, not args.no_instrument)
+        attach_traffic(name, r["calls"])
         del d
         torch.cuda.empty_cache()
         extra[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
