@@ -218,10 +218,10 @@ def describe(wl):
     return d
 
 
-def traffic_for(name, call):
-    """HBM bytes per call of `call` measured with rocprofv3 PMC counters
-    (profiles/traffic_<workload>.json, written by profsum --traffic), or None
-    when the record is missing or was taken on other kernel sources."""
+def traffic_record(name, call):
+    """The traffic record of `call` (profiles/traffic_<workload>.json, written
+    by profsum --traffic from rocprofv3 PMC counters), or None when it is
+    missing or was taken on other kernel sources."""
     path = os.path.join(ROOT, "profiles", "traffic_%s.json" % name)
     if not os.path.exists(path):
         return None
@@ -230,17 +230,26 @@ def traffic_for(name, call):
     rec = t.get("calls", {}).get(call)
     if rec is None or rec.get("source_hash") != source_hash(call):
         return None
-    return rec["bytes_per_call"]
+    return rec
+
+
+def traffic_for(name, call):
+    """Measured HBM bytes per call of `call`, or None (see traffic_record)."""
+    rec = traffic_record(name, call)
+    return None if rec is None else rec["bytes_per_call"]
 
 
 def attach_traffic(name, calls):
-    """Add the measured HBM bytes per call (and their ratio to the
-    algorithmic bytes) to every call that has a current traffic record."""
+    """Add the measured HBM bytes per call to every call that has a current
+    traffic record, with their ratio to the algorithmic bytes of the same
+    dispatches (the counter run's own, prompt included) when the record
+    holds them."""
     for call, c in calls.items():
-        t = traffic_for(name, call)
-        if t is not None:
-            c["measured_bytes_per_call"] = int(t)
-            c["measured_over_alg"] = round(t / c["bytes_per_call"], 4)
+        rec = traffic_record(name, call)
+        if rec is not None:
+            c["measured_bytes_per_call"] = int(rec["bytes_per_call"])
+            if "measured_over_alg" in rec:
+                c["measured_over_alg"] = rec["measured_over_alg"]
 
 
 def cpu_baseline(dec, wl, min_s=10.0):

@@ -140,17 +140,43 @@ def traffic(fetch_dir: str, write_dir: str, calib_bytes: int, workload: str) -> 
                 calls=calls)
 
 
+def attach_alg(rec: dict, log_path: str) -> None:
+    """Add trafficrun's algorithmic bytes per dispatch (its last JSON line)
+    to each call of a traffic record, with the measured/algorithmic ratio;
+    the dispatch counts of the two must agree."""
+    alg = None
+    with open(log_path) as fh:
+        for line in fh:
+            line = line.strip()
+            if line.startswith("{") and "alg_bytes_per_dispatch" in line:
+                alg = json.loads(line)
+    if alg is None:
+        raise SystemExit("no algorithmic-bytes line in %s" % log_path)
+    for call, c in rec["calls"].items():
+        if call not in alg["alg_bytes_per_dispatch"]:
+            continue
+        n = alg["dispatches"][call]
+        got = {k["dispatches"] for k in c["kernels"]}
+        if got != {n}:
+            raise SystemExit("%s: %s dispatches counted, %d run" % (call, sorted(got), n))
+        c["alg_bytes_per_dispatch"] = alg["alg_bytes_per_dispatch"][call]
+        c["measured_over_alg"] = round(c["bytes_per_call"] / c["alg_bytes_per_dispatch"], 4)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("dirs", nargs="+")
     ap.add_argument("--traffic", help="write the per-call traffic record to this JSON file")
     ap.add_argument("--workload", default="")
     ap.add_argument("--calib-bytes", type=int, default=1 << 30)
+    ap.add_argument("--alg", help="trafficrun's output: add its algorithmic bytes per dispatch")
     args = ap.parse_args(argv)
     if args.traffic:
         if len(args.dirs) != 2:
             raise SystemExit("--traffic takes the FETCH_SIZE and the WRITE_SIZE result directories")
         rec = traffic(args.dirs[0], args.dirs[1], args.calib_bytes, args.workload)
+        if args.alg:
+            attach_alg(rec, args.alg)
         with open(args.traffic, "w") as fh:
             json.dump(rec, fh, indent=1)
         print(json.dumps(rec, indent=1))
