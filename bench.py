@@ -252,12 +252,42 @@ def attach_traffic(name, calls):
                 c["measured_over_alg"] = rec["measured_over_alg"]
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(dec, wl, min_s=10.0):
-    """The fp64 oracle timed on this host, on a bounded sample of the same
-    workload: one problem's share of a decode step (its candidates' base
-    attention, helper attention and logit rows) at a time, problem after
-    problem and step after step, until at least `min_s` seconds of oracle
-    time; scaled to whole steps. Host copies are made outside the timing."""
+    """The fp64 oracle timed on this host with all its OpenMP threads and
+    with one thread (a reported baseline, not a target); see
+    oracle_sample for the sample. `value` is the all-threads rate."""
+    import oracle
+    n_all = oracle.threads()
+    steps, secs, desc, done, problems = oracle_sample(dec, wl, min_s)
+    oracle.set_threads(1)
+    try:
+        steps1, secs1, _, done1, _ = oracle_sample(dec, wl, min_s)
+    finally:
+        oracle.set_threads(n_all)
+    return dict(value=round(steps / secs, 6), unit="steps/s", cores=n_all, kind="oracle",
+                single_thread_value=round(steps1 / secs1, 6), nproc=os.cpu_count(), cpu_model=cpu_model(),
+                sample="%d problem-steps of %d problems per step (%s), %.1f s of oracle time on %d threads; "
+                       "%d problem-steps, %.1f s on one thread"
+                % (done, problems, "; ".join(desc), secs, n_all, done1, secs1))
+
+
+def oracle_sample(dec, wl, min_s):
+    """One problem's share of a decode step (its candidates' base attention,
+    helper attention and logit rows) at a time, problem after problem and
+    step after step, until at least `min_s` seconds of oracle time. Returns
+    (whole steps, seconds, description, problem-steps, problems per step).
+    Host copies are made outside the timing."""
     import numpy as np
 
     import oracle
@@ -311,10 +341,7 @@ def cpu_baseline(dec, wl, min_s=10.0):
                 break
         if secs >= min_s:
             break
-    steps = done / problems
-    return dict(value=round(steps / secs, 6), unit="steps/s", cores=oracle.threads(), kind="oracle",
-                sample="%d problem-steps of %d problems per step (%s), %.1f s of oracle time"
-                % (done, problems, "; ".join(desc), secs))
+    return done / problems, secs, desc, done, problems
 
 
 def main():
