@@ -45,7 +45,15 @@ namespace kvr {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kRoundVecs = 10 * kThreads;  // 8-logit vectors per workgroup per round (entropy alone)
+constexpr int kU = 10;                      // 8-logit vectors per thread per round (entropy alone)
+constexpr int kRoundVecs = kU * kThreads;   // vectors per workgroup per round
+// Whole-row workgroups: when a call has at least one row per CU and long
+// rows, each row gets one workgroup of kRowThreads threads that reduces it
+// completely (entropy and detector in the same kernel, no split partials
+// and no merge launch).
+constexpr int kRowThreads = 1024;
+constexpr int kRowMinRows = 256;
+constexpr int kRowMinVecs = 8 * kRowThreads;
 constexpr float kNegInf = -__builtin_huge_valf();
 
 struct Tri {
@@ -383,15 +391,15 @@ __device__ __forceinline__ int batch_set(const EntropyBatch &b, int g) {
   return k;
 }
 
-// One workgroup per (split, global row of the batch).
+// One workgroup of NT threads per (split, global row of the batch).
 // VEC = true: 16-byte loads of 8 elements (row starts 16-byte aligned).
 // SAMPLE = true: also collect the split's top_k candidates (always writes
 // the split's partials, even unsplit rows, for the sampling merge).
-template <typename T, bool VEC, bool SAMPLE>
-__global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
-  __shared__ Tri part[kThreads / kWave];
-  __shared__ uint64_t cand[SAMPLE ? (kThreads / kWave) * kCandCap : 1];
-  __shared__ int cand_n[kThreads / kWave];
+template <typename T, bool VEC, bool SAMPLE, int NT = kThreads>
+__global__ __launch_bounds__(NT) void entropy_kernel(EntropyBatch b) {
+  __shared__ Tri part[NT / kWave];
+  __shared__ uint64_t cand[SAMPLE ? (NT / kWave) * kCandCap : 1];
+  __shared__ int cand_n[NT / kWave];
   const int bset = batch_set(b, blockIdx.y);
   const EntropyParams &p = b.set[bset];
   const int row = blockIdx.y - b.row0[bset];
@@ -411,7 +419,9 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
     // round overlaps its later loads. Entropy alone: 10, so that a split of
     // the 7B / 1.5B vocabularies over 8 workgroups per row is one round. With
     // the sampler: 8, whose lower register count keeps 4 waves per SIMD.
-    constexpr int U = SAMPLE ? 8 : kRoundVecs / kThreads;
+    // Whole-row workgroups keep 10 (20, one round over a 152k bf16 row,
+    // measured 3% slower).
+    constexpr int U = SAMPLE ? 8 : kU;
     const int nvec = p.V / 8;
     const int per = (nvec + splits - 1) / splits;
     const int v0 = split * per;
@@ -421,9 +431,9 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
     const rsrc_t rr = row_rsrc(x, (uint32_t)v1 * 8u * (uint32_t)sizeof(T));
     // The loop bound is the same for every thread (lanes past the end load
     // zeros and skip them), so waves offer sampler candidates in lockstep.
-    for (int b0 = v0; b0 < v1; b0 += U * kThreads) {
+    for (int b0 = v0; b0 < v1; b0 += U * NT) {
       const int base = b0 + tid;
-      const bool full = b0 + U * kThreads <= v1;
+      const bool full = b0 + U * NT <= v1;
       // The loads are issued in vector order (the scheduling barriers keep
       // the compiler from reordering them), so that each fold below waits
       // only for its own vector; the asm statement keeps a load whose value
@@ -431,7 +441,7 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
       Vec8<T> w[U];
 #pragma unroll
       for (int u = 0; u < U; u++) {
-        w[u].load(rr, base + u * kThreads);
+        w[u].load(rr, base + u * NT);
         __builtin_amdgcn_sched_barrier(0);
       }
       asm volatile("" ::: "memory");
@@ -443,7 +453,7 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
           for (int u = 0; u < U; u++) {
             float a[8];
             w[u].get(a);
-            if (base + u * kThreads < v1)
+            if (base + u * NT < v1)
 #pragma unroll
               for (int e = 0; e < 8; e++) mx = vmax(mx, a[e]);
           }
@@ -454,7 +464,7 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
       for (int u = 0; u < U; u++) {
         float a[8];
         w[u].get(a);
-        const int v = base + u * kThreads;
+        const int v = base + u * NT;
         const bool ok = full || v < v1;
         if constexpr (SAMPLE) cand_offer(cs, p.top_k, lane, a, (uint32_t)v * 8u, ok ? 8 : 0);
         if (ok) tri_fold8(t, a, c);
@@ -480,7 +490,7 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
     const int e1 = min(e0 + per, p.V);
     // Every thread runs the same number of iterations so that whole waves
     // offer candidates together.
-    for (int eb = e0; eb < e1; eb += kThreads) {
+    for (int eb = e0; eb < e1; eb += NT) {
       const int e = eb + tid;
       const bool has = e < e1;
       float a[8] = {kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf, kNegInf};
@@ -507,7 +517,7 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
   if constexpr (SAMPLE) {
     // First wave: the k best of the waves' lists go to the workspace.
     if (wave != 0) return;
-    constexpr int NW = kThreads / kWave;
+    constexpr int NW = NT / kWave;
     int off[NW + 1];
     off[0] = 0;
 #pragma unroll
@@ -530,7 +540,7 @@ __global__ __launch_bounds__(kThreads) void entropy_kernel(EntropyBatch b) {
     if (wave != 0) return;
     Tri r = part[0];
 #pragma unroll
-    for (int w = 1; w < kThreads / kWave; w++) r = tri_merge(r, part[w]);
+    for (int w = 1; w < NT / kWave; w++) r = tri_merge(r, part[w]);
     if (splits == 1) {
       const float H = finish_entropy(r);
       if (lane == 0) p.H[row] = H;
@@ -641,7 +651,9 @@ __global__ __launch_bounds__(kWave) void sample_merge(EntropyParams p) {
 
 }  // namespace
 
-int entropy_splits(int R, int V) {
+static bool row_groups(int R, int V) { return R >= kRowMinRows && V / 8 >= kRowMinVecs; }
+
+static int split_rule(int R, int V) {
   // Enough workgroups to cover the chip (~1024), but at least 1024 vectors of
   // 8 logits per workgroup; and, when the rows alone fill the chip, still no
   // more than one round of the vector loop per workgroup (measured: 256 rows
@@ -657,6 +669,8 @@ int entropy_splits(int R, int V) {
   return (int)s;
 }
 
+int entropy_splits(int R, int V) { return row_groups(R, V) ? 1 : split_rule(R, V); }
+
 size_t entropy_workspace_bytes(int R, int V) {
   const int s = entropy_splits(R, V);
   if (s == 1) return 0;
@@ -664,7 +678,7 @@ size_t entropy_workspace_bytes(int R, int V) {
 }
 
 int sample_splits(int R, int V, int top_k) {
-  int s = entropy_splits(R, V);
+  int s = split_rule(R, V);
   const int maxs = kMergeEntries / (top_k > 0 ? top_k : 1);
   return s < maxs ? s : maxs;
 }
@@ -675,8 +689,9 @@ size_t sample_workspace_bytes(int R, int V, int top_k) {
 }
 
 template <typename T, bool VEC>
-static void launch_split(const EntropyBatch &b, bool sample, dim3 grid, hipStream_t stream) {
+static void launch_split(const EntropyBatch &b, bool sample, bool rows, dim3 grid, hipStream_t stream) {
   if (sample) hipLaunchKernelGGL((entropy_kernel<T, VEC, true>), grid, dim3(kThreads), 0, stream, b);
+  else if (rows) hipLaunchKernelGGL((entropy_kernel<T, VEC, false, kRowThreads>), grid, dim3(kRowThreads), 0, stream, b);
   else hipLaunchKernelGGL((entropy_kernel<T, VEC, false>), grid, dim3(kThreads), 0, stream, b);
 }
 
@@ -686,15 +701,20 @@ static hipError_t launch_partials(const EntropyBatch &b, bool sample, hipStream_
   const EntropyParams &p0 = b.set[0];
   const size_t esz = p0.dtype == 0 ? 4 : 2;
   bool vec = true;
-  for (int k = 0; k < b.nsets; k++)
+  int vmin = p0.V;
+  for (int k = 0; k < b.nsets; k++) {
     vec = vec && ((uintptr_t)b.set[k].logits % 16 == 0) && ((size_t)b.set[k].ld * esz % 16 == 0);
-  const dim3 grid(p0.splits, b.row0[b.nsets]);
+    vmin = b.set[k].V < vmin ? b.set[k].V : vmin;
+  }
+  const int R = b.row0[b.nsets];
+  const bool rows = p0.splits == 1 && row_groups(R, vmin);
+  const dim3 grid(p0.splits, R);
   if (p0.dtype == 0) {
-    if (vec) launch_split<float, true>(b, sample, grid, stream);
-    else launch_split<float, false>(b, sample, grid, stream);
+    if (vec) launch_split<float, true>(b, sample, rows, grid, stream);
+    else launch_split<float, false>(b, sample, rows, grid, stream);
   } else {
-    if (vec) launch_split<bf16_t, true>(b, sample, grid, stream);
-    else launch_split<bf16_t, false>(b, sample, grid, stream);
+    if (vec) launch_split<bf16_t, true>(b, sample, rows, grid, stream);
+    else launch_split<bf16_t, false>(b, sample, rows, grid, stream);
   }
   return hipGetLastError();
 }

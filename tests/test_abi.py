@@ -92,16 +92,22 @@ def test_entropy_batch_rejects_bad_arguments_on_host():
         return arr
 
     f, ws = kvr.lib.kvr_logit_entropy_batch, kvr.lib.kvr_logit_entropy_batch_workspace_size
-    two = sets((1, 128, 152064, 152064, 1.0), (1, 128, 151936, 151936, 1.0))
-    # Both vocabularies over one split plan: 256 rows x 8 splits of 16-byte partials.
-    assert ws(two, 2) == 256 * 8 * 16
+    # 256 long rows (both 128-row vocabularies of the default step): one
+    # whole-row workgroup per row, no split partials, no workspace.
+    assert ws(sets((1, 128, 152064, 152064, 1.0), (1, 128, 151936, 151936, 1.0)), 2) == 0
+    # 2 x 64 rows share one split plan: 128 rows x 8 splits of 16-byte partials.
+    two = sets((1, 64, 152064, 152064, 1.0), (1, 64, 151936, 151936, 1.0))
+    assert ws(two, 2) == 128 * 8 * 16
     assert f(two, 2, None, 0, None) == -4
-    assert f(two, 2, 16, 256 * 8 * 16 - 1, None) == -4
+    assert f(two, 2, 16, 128 * 8 * 16 - 1, None) == -4
     assert f(None, 2, None, 0, None) == -1
     for n in (0, 5):
         assert f(two, n, None, 0, None) == -1 and "nsets" in kvr.lib.kvr_last_error().decode()
     # The size query reads shapes only.
-    assert kvr.logit_entropy_batch_workspace_size([(128, 152064), (128, 151936)]) == 256 * 8 * 16
+    assert kvr.logit_entropy_batch_workspace_size([(128, 152064), (128, 151936)]) == 0
+    assert kvr.logit_entropy_batch_workspace_size([(64, 152064), (64, 151936)]) == 128 * 8 * 16
+    assert kvr.logit_entropy_workspace_size(300, 152064) == 0  # whole-row workgroups
+    assert kvr.logit_entropy_workspace_size(128, 152064) == 128 * 8 * 16
     assert kvr.logit_entropy_batch_workspace_size([(3, 10)]) == 0
     mixed = sets((1, 4, 10, 10, 1.0), (0, 4, 10, 10, 1.0))
     assert f(mixed, 2, None, 0, None) == -1 and "dtype" in kvr.lib.kvr_last_error().decode()

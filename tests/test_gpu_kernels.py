@@ -391,6 +391,7 @@ ENT_CASES = [
     (5, 152064, 152072, torch.bfloat16, 0.1),
     (300, 1000, 1003, torch.bfloat16, 1.0),
     (2, 50000, 50000, torch.float32, 5.0),
+    (300, 152064, 152064, torch.bfloat16, 3.0),  # whole-row workgroups
 ]
 
 
@@ -432,6 +433,9 @@ ENT_BATCH_CASES = [
      (5, 2048, 2048, 2.0, 0.8, True), (300, 8000, 8000, 3.0, 1.0, False)],
     [(3, 7, 9, 2.0, 1.0, False), (1, 1, 1, 1.0, 1.0, False), (4, 50000, 50003, 5.0, 1.0, True)],
     [(32, 152064, 152064, 3.0, 1.0, True)],
+    # At least 256 long rows: one whole-row workgroup per row; the second set's
+    # stride is not a multiple of 16 bytes, so every set takes the scalar loads.
+    [(200, 152064, 152064, 3.0, 1.0, True), (57, 100000, 100003, 1.0, 1.25, True)],
 ]
 
 
