@@ -322,6 +322,7 @@ __device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st, f
 // next chunk's loads are in flight while the current one is computed; the
 // appended token (slot n-1) is a final one-key tile read from k_new/v_new.
 constexpr size_t kBaseLdsFloor = 26 * 1024;  // see the evicted-cache launch
+constexpr int kFastPieces = 4;  // split partials per row merged with batched LDS reads
 
 template <int D, bool MERGE, int TILES, int DEPTH>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void attn_cache_bf16(AttnParams p) {
@@ -500,6 +501,50 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
         auto rec = [&](int k) -> const float * {
           return k < pf ? smem + k * p.merge_blk + row * RF : rbase + k * rstride + row * RF;
         };
+        if (npieces <= kFastPieces && npieces <= pf) {
+          // Every piece is in LDS: all of its reads are issued before any is
+          // used, so the row's merge costs one LDS round trip.
+          float rm[kFastPieces], rs[kFastPieces];
+          uint32_t hv[kFastPieces][NB / 2];
+#pragma unroll
+          for (int k = 0; k < kFastPieces; k++) {
+            if (k < npieces) {
+              const float *r = smem + k * p.merge_blk + row * RF;
+              const float2_t ms = *reinterpret_cast<const float2_t *>(r);
+              rm[k] = ms.x;
+              rs[k] = ms.y;
+              if constexpr (D == 128) {
+                const u32x4 x = *reinterpret_cast<const u32x4 *>(r + 4 + r16 * (NB / 2));
+                hv[k][0] = x.x; hv[k][1] = x.y; hv[k][2] = x.z; hv[k][3] = x.w;
+              } else {
+                const u32x2 x = *reinterpret_cast<const u32x2 *>(r + 4 + r16 * (NB / 2));
+                hv[k][0] = x.x; hv[k][1] = x.y;
+              }
+            } else {
+              rm[k] = kNegInf;
+              rs[k] = 0.0f;
+#pragma unroll
+              for (int b = 0; b < NB / 2; b++) hv[k][b] = 0u;
+            }
+          }
+          float M = mi;
+#pragma unroll
+          for (int k = 0; k < kFastPieces; k++) M = fmaxf(M, rm[k]);
+          const float wown = fast_exp2(mi - M);
+          zi *= wown;
+#pragma unroll
+          for (int b = 0; b < NB; b++) o[b][i] *= wown;
+#pragma unroll
+          for (int k = 0; k < kFastPieces; k++) {
+            const float w = rm[k] == kNegInf ? 0.0f : rs[k] * fast_exp2(rm[k] - M);
+            zi += w;
+#pragma unroll
+            for (int b = 0; b < NB / 2; b++) {
+              o[2 * b][i] += f16_lo(hv[k][b]) * w;
+              o[2 * b + 1][i] += f16_hi(hv[k][b]) * w;
+            }
+          }
+        } else {
         float M = mi;
         for (int k = 0; k < npieces; k++) M = fmaxf(M, rec(k)[0]);
         const float wown = fast_exp2(mi - M);
@@ -525,6 +570,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
             o[2 * b][i] += f16_lo(hv[b]) * w;
             o[2 * b + 1][i] += f16_hi(hv[b]) * w;
           }
+        }
         }
       }
     }
