@@ -39,12 +39,14 @@ CALL_SOURCES = {
     "entropy": ("entropy.hip", "kvr_device.h"),
 }
 
-# Kernels launched by one call of each hot-path entry point, by call name.
+# Kernels launched by one call of each hot-path entry point, by call name; a
+# pattern starting with "?" names a kernel the call launches only for some
+# shapes (the entropy merge, absent when whole rows go to one workgroup).
 CALL_KERNELS = {
     "base_attn": (r"attn_cache_bf16<\d+, false",),
     "helper_attn": (r"attn_prefix_bf16<", r"attn_cache_bf16<\d+, true"),
     "evict": (r"evict_topb_kernel",),
-    "entropy": (r"entropy_kernel<", r"entropy_merge"),
+    "entropy": (r"entropy_kernel<", r"?entropy_merge"),
 }
 
 
@@ -122,7 +124,10 @@ def traffic(fetch_dir: str, write_dir: str, calib_bytes: int, workload: str) -> 
     for call, pats in CALL_KERNELS.items():
         parts, rd, wr = [], 0.0, 0.0
         for p in pats:
-            ks = [k for k in fetch if re.search(p, k) and k in write]
+            optional = p.startswith("?")
+            ks = [k for k in fetch if re.search(p.lstrip("?"), k) and k in write]
+            if optional and not ks:
+                continue
             if len(ks) != 1:
                 break
             k = ks[0]

@@ -5,9 +5,8 @@
 Runs a calibration copy (three dispatches of a 1 GiB bf16 -> fp16 conversion:
 1 GiB read and 1 GiB written each, the reference that profsum scales the
 FETCH_SIZE / WRITE_SIZE counters by), then the workload's prompt and N decode
-steps of base attention (with its evictions) and helper attention, the calls
-of the decode step that move more than 99% of its bytes. The entropy calls
-are left out of these passes; their bytes are measured on their own.
+steps of the whole hot path: base attention (with its evictions), helper
+attention and the batched logit-entropy call.
 Run it under one `rocprofv3 --pmc FETCH_SIZE` and one `--pmc WRITE_SIZE` pass
 and give both result directories to `profsum --traffic`. N defaults to the
 workload's decode steps, the benchmark's timed window, so the per-dispatch
@@ -84,6 +83,9 @@ def main(argv=None) -> None:
         if wl.helper:
             dec.helper_token(i, si)
             count("helper_attn", acc.helper_attn_bytes(wl, dec.hlen_host[i]))
+        if wl.logits:
+            dec.entropy(si)
+            count("entropy", acc.entropy_bytes(wl))
         if (i + 1) % 512 == 0:
             torch.cuda.synchronize()
             print("[%s] %d steps (%.1fs)" % (wl.name, i + 1, time.time() - t0), flush=True)
