@@ -145,6 +145,16 @@ def fit_line(xs, ys):
     return my - b * mx, b
 
 
+def crossover_point(t, a, b, Bp, best):
+    """Where evicted decode at t ms per step meets the fitted full-KV line
+    t(l) = a + b l: alpha = t / t(B') - 1 and l* = (t - a) / b, with the
+    speed-up over full KV at each measured length (best: l -> ms)."""
+    t_bp = a + b * Bp
+    return dict(ms=round(t, 5), alpha=round(t / t_bp - 1.0, 3),
+                ell_star=round((t - a) / b, 1),
+                speedup={str(k): round(v / t, 3) for k, v in best.items()})
+
+
 def measure(S=16, B=512, W=128, buffer=128,
             lengths=(640, 1024, 2048, 3072, 4096, 6144, 8192, 12288, 16384)):
     L, Hq, Hkv, D = QWEN7B["L"], QWEN7B["Hq"], QWEN7B["Hkv"], QWEN7B["D"]
@@ -162,9 +172,7 @@ def measure(S=16, B=512, W=128, buffer=128,
     t_rkv = t_scored + t_red + t_evict
 
     def cross(t):
-        return dict(ms=round(t, 5), alpha=round(t / t_bp - 1.0, 3),
-                    ell_star=round((t - a) / b, 1),
-                    speedup={str(k): round(v / t, 3) for k, v in best.items()})
+        return crossover_point(t, a, b, Bp, best)
 
     return dict(shape=dict(S=S, L=L, Hq=Hq, Hkv=Hkv, D=D, B=B, W=W, buffer=buffer, B_prime=Bp),
                 full_ms={str(k): dict(context_path=round(v[0], 5), cache_kernel=round(v[1], 5))
