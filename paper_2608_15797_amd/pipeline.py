@@ -159,7 +159,7 @@ class Decoder:
 
     # -- one token ------------------------------------------------------------
     def base_token(self, t: int, si: StepInputs, stream=None, on_scored=None,
-                   timers=None, evict_log=None) -> bool:
+                   timers=None, evict_log=None, only=None) -> bool:
         """Append + attend (+ score) for token t; evict if the cache overflows.
         Returns True when an eviction ran. `on_scored(t)` (tests) runs between
         the attention and the eviction. With `evict_log` (a list), each
@@ -167,14 +167,14 @@ class Decoder:
         slot (read back from the kept sets: a synchronising copy, for
         accounting outside timed regions)."""
         b = self.wl.base
-        with _timer(timers, "base_attn", stream):
+        with _timer(timers, "base_attn", stream, only):
             kvr.decode_attn(self.bcache, self.blen[t], si.bq, self.bout, self.bscale,
                             k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,
                             scores=self.scores, stream=stream)
         if on_scored is not None:
             on_scored(t)
         if self.blen_host[t] > b.B + b.buffer:
-            with _timer(timers, "evict", stream):
+            with _timer(timers, "evict", stream, only):
                 kvr.evict_topb(self.bcache, self.blen[t], self.scores, self.policy,
                                kept=self.kept, stream=stream)
             if evict_log is not None:
@@ -183,46 +183,48 @@ class Decoder:
             return True
         return False
 
-    def helper_token(self, step: int, si: StepInputs, stream=None, timers=None) -> None:
+    def helper_token(self, step: int, si: StepInputs, stream=None, timers=None, only=None) -> None:
         h = self.wl.helper
-        with _timer(timers, "helper_attn", stream):
+        with _timer(timers, "helper_attn", stream, only):
             kvr.decode_attn(self.hcache, self.hlen[step], si.hq, self.hout, h.softmax_scale,
                             k_new=si.hk, v_new=si.hv, prefix=self.prefix, workspace=self.hws,
                             stream=stream)
 
-    def entropy(self, si: StepInputs, stream=None, timers=None) -> None:
+    def entropy(self, si: StepInputs, stream=None, timers=None, only=None) -> None:
         """Entropies of every logit set of the step in one batched call."""
         if not si.logits:
             return
         sets = [kvr.LogitSet(lg, self.H[w], self.wl.logits[w].V,
                              detector=self.detector if w == 0 else None)
                 for w, lg in enumerate(si.logits)]
-        with _timer(timers, "entropy", stream):
+        with _timer(timers, "entropy", stream, only):
             kvr.logit_entropy_batch(sets, workspace=self.ews_batch, stream=stream)
 
     def prompt(self, stream=None) -> None:
         for t in range(self.T_prompt):
             self.base_token(t, self.inputs(t), stream)
 
-    def step(self, step: int, stream=None, timers=None, evict_log=None) -> None:
+    def step(self, step: int, stream=None, timers=None, evict_log=None, only=None) -> None:
         """Decode step `step` (0-based, after the prompt): the whole hot path.
-        With `timers` (a dict), each call is bracketed by a pair of timing
-        events on the launch stream, appended under its name; `evict_log` as
-        for base_token."""
+        With `timers` (a dict), each call (or only the call named `only`) is
+        bracketed by a pair of timing events on the launch stream, appended
+        under its name; `evict_log` as for base_token."""
         t = self.T_prompt + step
         si = self.inputs(t)
         if self.wl.base:
-            self.base_token(t, si, stream, timers=timers, evict_log=evict_log)
+            self.base_token(t, si, stream, timers=timers, evict_log=evict_log, only=only)
         if self.wl.helper:
-            self.helper_token(step, si, stream, timers=timers)
-        self.entropy(si, stream, timers=timers)
+            self.helper_token(step, si, stream, timers=timers, only=only)
+        self.entropy(si, stream, timers=timers, only=only)
 
 
 class _timer:
-    """Context manager recording start/end events around one library call."""
+    """Context manager recording start/end events around one library call
+    (when timers is a dict and `only` is None or names this call)."""
 
-    def __init__(self, timers, key, stream):
-        self.timers, self.key, self.stream = timers, key, stream
+    def __init__(self, timers, key, stream, only=None):
+        self.timers = timers if (only is None or only == key) else None
+        self.key, self.stream = key, stream
 
     def __enter__(self):
         if self.timers is not None:

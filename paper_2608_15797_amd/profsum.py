@@ -1,8 +1,8 @@
 """Summarise rocprofv3 result databases as short text.
 
-    python -m paper_2608_15797_amd.profsum DIR [DIR ...]
+    python -m paper_2608_15797_amd.profsum [--window A B] DIR [DIR ...]
     python -m paper_2608_15797_amd.profsum --traffic OUT.json --workload NAME \
-        --calib-bytes N FETCH_DIR WRITE_DIR
+        --calib-bytes N [--window A B] FETCH_DIR WRITE_DIR
 
 The first form prints, for every *_results.db under each DIR, per kernel the
 dispatch count and average duration, and the per-dispatch average of every
@@ -18,6 +18,12 @@ entry carries a hash of its kernel sources (CALL_SOURCES) so that a reader
 can tell whether it was taken on the kernels it runs. Per-dispatch averages
 run over every dispatch of the profiled program, so the passes should run
 the same steps as the measurement they are compared with.
+
+--window A B restricts both forms to the library dispatches issued between
+marker dispatch A and marker dispatch B (0-based, in issue order); the
+markers are the one-thread spin kernels (torch.cuda._sleep) that bench.py and
+trafficrun launch around each of their passes. The calibration copy is
+always taken from the whole run.
 """
 from __future__ import annotations
 
@@ -63,21 +69,99 @@ def keep(name: str) -> bool:
     return "kvr" in name or "copy" in name.lower()
 
 
+def is_marker(name: str) -> bool:
+    return "spin_kernel" in name
+
+
+def _cols(c, view):
+    return [x[1] for x in c.execute("pragma table_info(%s)" % view)]
+
+
+def _pick(cols, *names):
+    low = {x.lower(): x for x in cols}
+    for n in names:
+        if n in low:
+            return low[n]
+    return None
+
+
+def dispatch_rows(db: str) -> list[dict]:
+    """Every kernel dispatch of a kernel-trace database as {order, name, dur_ns},
+    in issue order."""
+    c = sqlite3.connect(db)
+    for view in ("kernels", "kernel_dispatch", "rocpd_kernel_dispatch"):
+        cols = _cols(c, view)
+        if cols:
+            break
+    else:
+        raise SystemExit("%s: no kernel dispatch table" % db)
+    name = _pick(cols, "name", "kernel_name")
+    start, end = _pick(cols, "start", "start_timestamp"), _pick(cols, "end", "end_timestamp")
+    order = _pick(cols, "dispatch_id", "correlation_id", "id")
+    if not (name and start and end and order):
+        raise SystemExit("%s: unexpected columns %s" % (db, cols))
+    rows = [dict(order=r[0], name=r[1] or "", dur_ns=float(r[3]) - float(r[2]))
+            for r in c.execute('select "%s", "%s", "%s", "%s" from %s' % (order, name, start, end, view))]
+    rows.sort(key=lambda r: r["order"])
+    return rows
+
+
+def window_orders(rows: list[dict], window) -> tuple:
+    """(first, last) issue order strictly between marker dispatches A and B."""
+    if window is None:
+        return None
+    marks = [r["order"] for r in rows if is_marker(r["name"])]
+    a, b = window
+    if b >= len(marks):
+        raise SystemExit("window %s: only %d markers in the run" % (window, len(marks)))
+    return marks[a], marks[b]
+
+
+def in_window(order, bounds) -> bool:
+    return bounds is None or bounds[0] < order < bounds[1]
+
+
+def window_stats(db: str, window) -> list[str]:
+    """Per-kernel dispatch count and average duration within a marker window."""
+    rows = dispatch_rows(db)
+    bounds = window_orders(rows, window)
+    agg = collections.defaultdict(lambda: [0.0, 0])
+    for r in rows:
+        if keep(r["name"]) and in_window(r["order"], bounds):
+            agg[r["name"]][0] += r["dur_ns"]
+            agg[r["name"]][1] += 1
+    return ["duration  %-78s calls %7d  avg_us %10.2f" % (n[:78], k, t / k / 1e3)
+            for n, (t, k) in sorted(agg.items(), key=lambda x: -x[1][0])]
+
+
 def _dbs(d: str) -> list[str]:
     return sorted(glob.glob(d + "/**/*_results.db", recursive=True))
 
 
-def counters(db: str) -> dict:
-    """{(tag, counter): (sum of values, dispatches)}; copies are tagged by grid."""
+def counters(db: str, window=None) -> dict:
+    """{(tag, counter): (sum of values, dispatches)}; copies are tagged by grid.
+    With a marker window, library kernels count only inside it (copies always)."""
     c = sqlite3.connect(db)
     cols = [x[1] for x in c.execute("pragma table_info(counters_collection)")]
     agg = collections.defaultdict(lambda: [0.0, 0])
     if not cols:
         return agg
-    for row in c.execute("select * from counters_collection"):
-        r = dict(zip(cols, row))
+    order = _pick(cols, "dispatch_id", "correlation_id")
+    rows = [dict(zip(cols, row)) for row in c.execute("select * from counters_collection")]
+    bounds = None
+    if window is not None:
+        if order is None:
+            raise SystemExit("%s: counters have no dispatch order column (%s)" % (db, cols))
+        marks = sorted({r[order] for r in rows if is_marker(r.get("kernel_name") or "")})
+        a, b = window
+        if b >= len(marks):
+            raise SystemExit("window %s: only %d markers in %s" % (window, len(marks), db))
+        bounds = (marks[a], marks[b])
+    for r in rows:
         name = r.get("kernel_name") or ""
         if not keep(name):
+            continue
+        if "copy" not in name.lower() and not in_window(r[order] if order else 0, bounds):
             continue
         tag = name
         if "copy" in name.lower():
@@ -100,19 +184,19 @@ def summarise(db: str) -> list[str]:
     return out
 
 
-def _per_dispatch(dirs: list[str], counter: str) -> dict:
+def _per_dispatch(dirs: list[str], counter: str, window=None) -> dict:
     per = {}
     for d in dirs:
         for db in _dbs(d):
-            for (tag, cn), (v, n) in counters(db).items():
+            for (tag, cn), (v, n) in counters(db, window).items():
                 if cn == counter:
                     per[tag] = (v / n, n)
     return per
 
 
-def traffic(fetch_dir: str, write_dir: str, calib_bytes: int, workload: str) -> dict:
-    fetch = _per_dispatch([fetch_dir], "FETCH_SIZE")
-    write = _per_dispatch([write_dir], "WRITE_SIZE")
+def traffic(fetch_dir: str, write_dir: str, calib_bytes: int, workload: str, window=None) -> dict:
+    fetch = _per_dispatch([fetch_dir], "FETCH_SIZE", window)
+    write = _per_dispatch([write_dir], "WRITE_SIZE", window)
     kib = calib_bytes / 1024.0
     cal = [t for t in write if t.startswith("copy ") and abs(write[t][0] - kib) <= 0.1 * kib]
     if len(cal) != 1 or cal[0] not in fetch:
@@ -146,9 +230,11 @@ def traffic(fetch_dir: str, write_dir: str, calib_bytes: int, workload: str) -> 
 
 
 def attach_alg(rec: dict, log_path: str) -> None:
-    """Add trafficrun's algorithmic bytes per dispatch (its last JSON line)
-    to each call of a traffic record, with the measured/algorithmic ratio;
-    the dispatch counts of the two must agree."""
+    """Add the profiled program's algorithmic bytes per dispatch (the last
+    JSON line of its output holding "alg_bytes_per_dispatch") to each call of
+    a traffic record, with the measured/algorithmic ratio; the dispatch
+    counts of the two must agree. The line's "window" (the decode steps it
+    covers) is copied to the record."""
     alg = None
     with open(log_path) as fh:
         for line in fh:
@@ -166,6 +252,8 @@ def attach_alg(rec: dict, log_path: str) -> None:
             raise SystemExit("%s: %s dispatches counted, %d run" % (call, sorted(got), n))
         c["alg_bytes_per_dispatch"] = alg["alg_bytes_per_dispatch"][call]
         c["measured_over_alg"] = round(c["bytes_per_call"] / c["alg_bytes_per_dispatch"], 4)
+    if "window" in alg:
+        rec["window"] = alg["window"]
 
 
 def main(argv=None):
@@ -174,12 +262,17 @@ def main(argv=None):
     ap.add_argument("--traffic", help="write the per-call traffic record to this JSON file")
     ap.add_argument("--workload", default="")
     ap.add_argument("--calib-bytes", type=int, default=1 << 30)
-    ap.add_argument("--alg", help="trafficrun's output: add its algorithmic bytes per dispatch")
+    ap.add_argument("--alg", help="output of the profiled program: add its algorithmic bytes per dispatch")
+    ap.add_argument("--window", nargs=2, type=int, metavar=("A", "B"),
+                    help="only the dispatches between marker dispatches A and B")
     args = ap.parse_args(argv)
+    window = tuple(args.window) if args.window else None
     if args.traffic:
         if len(args.dirs) != 2:
             raise SystemExit("--traffic takes the FETCH_SIZE and the WRITE_SIZE result directories")
-        rec = traffic(args.dirs[0], args.dirs[1], args.calib_bytes, args.workload)
+        rec = traffic(args.dirs[0], args.dirs[1], args.calib_bytes, args.workload, window)
+        if window is not None:
+            rec["marker_window"] = list(window)
         if args.alg:
             attach_alg(rec, args.alg)
         with open(args.traffic, "w") as fh:
@@ -188,8 +281,8 @@ def main(argv=None):
         return
     for d in args.dirs:
         for db in _dbs(d):
-            print("##", db)
-            for line in summarise(db):
+            print("##", db, "" if window is None else "(marker window %d-%d)" % window)
+            for line in (summarise(db) if window is None else window_stats(db, window)):
                 print(line)
 
 

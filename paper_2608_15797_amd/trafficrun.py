@@ -1,22 +1,20 @@
 """Program for the HBM byte-counter passes of the attention and eviction calls.
 
-    python -m paper_2608_15797_amd.trafficrun [--workload NAME] [--steps N]
+    python -m paper_2608_15797_amd.trafficrun [--workload NAME] [--steps K] [--warmup W]
 
 Runs a calibration copy (three dispatches of a 1 GiB bf16 -> fp16 conversion:
 1 GiB read and 1 GiB written each, the reference that profsum scales the
-FETCH_SIZE / WRITE_SIZE counters by), then the workload's prompt and N decode
-steps of the whole hot path: base attention (with its evictions), helper
-attention and the batched logit-entropy call.
-Run it under one `rocprofv3 --pmc FETCH_SIZE` and one `--pmc WRITE_SIZE` pass
-and give both result directories to `profsum --traffic`. N defaults to the
-workload's decode steps, the benchmark's timed window, so the per-dispatch
-averages cover the same mix of cache and suffix lengths (the prompt adds the
-same few hundred dispatches as in the benchmark's own run).
+FETCH_SIZE / WRITE_SIZE counters by), then the workload's prompt, the W warmup
+steps and the K decode steps that bench.py times for the same --steps and
+--warmup (same placement of the window), between two marker kernels. Run it
+under one `rocprofv3 --pmc FETCH_SIZE` and one `--pmc WRITE_SIZE` pass and
+give both result directories to `profsum --traffic --window 0 1`, so the
+per-dispatch averages cover exactly the timed window's dispatches.
 
 The last line printed is a JSON object with the algorithmic bytes per
-dispatch of every call over exactly the dispatches of this run (prompt
-included; eviction at the kept rows that changed slot, read back from each
-eviction's kept set), to set against the measured bytes per dispatch.
+dispatch of every call over exactly the window's dispatches (eviction at the
+kept rows that changed slot, read back from each eviction's kept set), to set
+against the measured bytes per dispatch, and the window itself.
 """
 from __future__ import annotations
 
@@ -43,18 +41,21 @@ def main(argv=None) -> None:
     import json
 
     from paper_2608_15797_amd import accounting as acc
+    from paper_2608_15797_amd.benchplan import Schedule, cycle_steps, place_window, window_stats
     from paper_2608_15797_amd.pipeline import Decoder
     from paper_2608_15797_amd.workloads import WORKLOADS
 
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
-    ap.add_argument("--workload", default="base7b_helper", choices=sorted(WORKLOADS))
-    ap.add_argument("--steps", type=int, default=0, help="decode steps (default: the workload's)")
+    ap.add_argument("--workload", default="base72b_helper", choices=sorted(WORKLOADS))
+    ap.add_argument("--steps", type=int, default=0, help="window steps (default: one whole cycle)")
+    ap.add_argument("--warmup", type=int, default=32)
     args = ap.parse_args(argv)
     calibration_copy()
     print("calibration copy done", flush=True)
-    wl = WORKLOADS[args.workload]
-    if args.steps:
-        wl = wl.with_(steps=args.steps)
+    wl0 = WORKLOADS[args.workload]
+    K = args.steps or cycle_steps(wl0)
+    s0 = place_window(wl0, K, args.warmup)
+    wl = wl0.with_(steps=s0 + K + 1)
     t0 = time.time()
     dec = Decoder(wl, device="cuda")
     alg = {}  # call -> [bytes, dispatches]
@@ -64,34 +65,42 @@ def main(argv=None) -> None:
         a[0] += nbytes
         a[1] += 1
 
-    def base(t, si):
-        moved = []
-        if dec.base_token(t, si, evict_log=moved):
-            b = wl.base
-            count("evict", acc.evict_bytes(wl, dec.blen_host[t], moved[0] / (b.S * b.L * b.Hkv)))
-        count("base_attn", acc.base_attn_bytes(wl, dec.blen_host[t]))
-
-    for t in range(dec.T_prompt):
-        base(t, dec.inputs(t))
-    torch.cuda.synchronize()
-    print("[%s] prompt (%d tokens) done" % (wl.name, dec.T_prompt), flush=True)
-    for i in range(wl.steps):
+    def step(i, counted):
         t = dec.T_prompt + i
         si = dec.inputs(t)
         if wl.base:
-            base(t, si)
+            moved = []
+            if dec.base_token(t, si, evict_log=moved) and counted:
+                b = wl.base
+                count("evict", acc.evict_bytes(wl, dec.blen_host[t], moved[0] / (b.S * b.L * b.Hkv)))
+            if counted:
+                count("base_attn", acc.base_attn_bytes(wl, dec.blen_host[t]))
         if wl.helper:
             dec.helper_token(i, si)
-            count("helper_attn", acc.helper_attn_bytes(wl, dec.hlen_host[i]))
+            if counted:
+                count("helper_attn", acc.helper_attn_bytes(wl, dec.hlen_host[i]))
         if wl.logits:
             dec.entropy(si)
-            count("entropy", acc.entropy_bytes(wl))
-        if (i + 1) % 512 == 0:
+            if counted:
+                count("entropy", acc.entropy_bytes(wl))
+
+    dec.prompt()
+    for i in range(s0 - args.warmup, s0):
+        step(i, False)
+    torch.cuda.synchronize()
+    print("[%s] prompt (%d tokens) + %d warmup steps done" % (wl.name, dec.T_prompt, args.warmup), flush=True)
+    torch.cuda._sleep(1)
+    for i in range(s0, s0 + K):
+        step(i, True)
+        if (i - s0 + 1) % 128 == 0:
             torch.cuda.synchronize()
-            print("[%s] %d steps (%.1fs)" % (wl.name, i + 1, time.time() - t0), flush=True)
+            print("[%s] %d steps (%.1fs)" % (wl.name, i - s0 + 1, time.time() - t0), flush=True)
+    torch.cuda._sleep(1)
     torch.cuda.synchronize()
     print("done", flush=True)
-    print(json.dumps({"workload": wl.name, "alg_bytes_per_dispatch": {k: int(round(v[0] / v[1])) for k, v in alg.items()},
+    wstat = window_stats(wl, Schedule(wl, s0 + K + 1), s0, K)
+    print(json.dumps({"workload": wl.name, "window": wstat,
+                      "alg_bytes_per_dispatch": {k: int(round(v[0] / v[1])) for k, v in alg.items()},
                       "dispatches": {k: v[1] for k, v in alg.items()}}), flush=True)
 
 

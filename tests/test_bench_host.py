@@ -1,5 +1,6 @@
-"""Host side of bench.py: the single-GPU guard and the per-step byte
-accounting it divides by the measured durations."""
+"""Host side of bench.py: the single-GPU guard, the placement of the timed
+window and the per-step byte accounting it divides by the measured
+durations."""
 import os
 import subprocess
 import sys
@@ -32,7 +33,7 @@ def _decoder_stub(wl):
 
 @pytest.mark.parametrize("name", ["base7b_helper", "base7b", "base72b_helper", "helper4k"])
 def test_step_bytes_calls(name):
-    import bench
+    from paper_2608_15797_amd import benchplan as bench
     wl = WORKLOADS[name]
     dec = _decoder_stub(wl)
     e = 2  # bf16 logits
@@ -56,3 +57,51 @@ def test_step_bytes_calls(name):
         assert evict_steps == 63
         # The default workload's two logit sets: 77.8 MB per step.
         assert logit_bytes == 128 * 152064 * 2 + 128 * 151936 * 2 + 2 * 128 * 4
+
+
+@pytest.mark.parametrize("name", ["base72b_helper", "base7b_helper", "base7b", "helper4k"])
+@pytest.mark.parametrize("K,W", [(20, 5), (1, 0), (33, 5), (100, 32), (0, 32)])
+def test_window_placement(name, K, W):
+    """The timed window holds an eviction preceded by min(W_policy - 1, K - 1)
+    score-streaming steps (with the eviction step, the observation window),
+    starts after its warmup, and a default window
+    (K = 0: one whole cycle) covers every base length of the eviction cycle
+    equally and the helper suffix cycle."""
+    from paper_2608_15797_amd.benchplan import Schedule, cycle_steps, place_window, window_stats
+    wl = WORKLOADS[name]
+    C = cycle_steps(wl)
+    K = K or C
+    s0 = place_window(wl, K, W)
+    assert s0 >= W
+    sch = Schedule(wl, s0 + K + 1)
+    st = window_stats(wl, sch, s0, K)
+    b, h = wl.base, wl.helper
+    if b:
+        ev = [i for i in range(s0, s0 + K) if sch.evicts(i)]
+        assert ev, "no eviction in the window"
+        lead = min(b.W - 1, K - 1)
+        assert ev[0] - s0 == lead
+        assert all(sch.scores(i) for i in range(ev[0] - lead, ev[0] + 1))
+        assert st["evictions_in_window"] == len(ev)
+    if K == C:
+        if b:
+            # Whole eviction periods: every live length of the cycle equally often.
+            ns = sorted(sch.base_n(i) for i in range(s0, s0 + K))
+            per = b.buffer + 1
+            assert ns == sorted(list(range(b.B + 1, b.B + b.buffer + 2)) * (K // per))
+            assert st["mean_base_len"] == pytest.approx(b.B + (b.buffer + 2) / 2)
+        if h:
+            assert set(sch.hlen_host[s0:s0 + K]) == set(range(1, h.scap + 1))
+    if h and K >= 20:
+        assert abs(st["mean_helper_suffix"] - (h.scap + 1) / 2) < 0.1 * h.scap
+
+
+def test_driver_window_on_the_72b_workload():
+    """The driver's --steps 20 --warmup 5 on the default workload: one
+    eviction at the last step, all 20 steps streaming window scores."""
+    from paper_2608_15797_amd.benchplan import Schedule, place_window, window_stats
+    wl = WORKLOADS["base72b_helper"]
+    s0 = place_window(wl, 20, 5)
+    st = window_stats(wl, Schedule(wl, s0 + 21), s0, 20)
+    assert st["evictions_in_window"] == 1 and st["score_steps_in_window"] == 20
+    assert abs(st["mean_helper_suffix"] - 256.5) < 5
