@@ -20,8 +20,10 @@
  *
  * Conventions shared by every entry point
  *   - All array pointers are DEVICE pointers owned by the caller. The library
- *     never allocates, frees or retains them, and keeps no global state: calls
- *     on different streams are independent when their buffers do not alias.
+ *     never allocates, frees or retains them, and keeps no global state (the
+ *     one exception is the device scratch of kvr_logit_entropy_batch_noalloc):
+ *     calls on different streams are independent when their buffers do not
+ *     alias.
  *   - Arrays are row-major with the innermost index last. Element types are
  *     float32 (KVR_F32) or bfloat16 (KVR_BF16); arithmetic is float32.
  *   - bfloat16 arrays and float32 vector arrays must be 16-byte aligned.
@@ -293,6 +295,30 @@ int kvr_logit_entropy_batch(const kvr_logit_set *sets, int32_t nsets, void *work
 /* Depends on the sets' dtype, R, V, ld and inv_temp only (their pointers
  * are not read); 0 when those are invalid. */
 size_t kvr_logit_entropy_batch_workspace_size(const kvr_logit_set *sets, int32_t nsets);
+
+/* Bytes of device scratch the library holds per GPU for
+ * kvr_logit_entropy_batch_noalloc (the largest workspace it accepts). */
+#define KVR_ENTROPY_SCRATCH_BYTES ((size_t)1 << 20)
+
+/*
+ * kvr_logit_entropy_batch_noalloc -- kvr_logit_entropy_batch without a caller
+ * workspace and without allocating anything: for callers that cannot call
+ * hipMalloc or pass fresh device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation). Same sets, results and
+ * errors as kvr_logit_entropy_batch.
+ *
+ * The split partials go to a device array of KVR_ENTROPY_SCRATCH_BYTES that
+ * the library holds on each GPU until the process ends (its address on a
+ * device is looked up on the first call made with that device current). A
+ * call whose workspace size (kvr_logit_entropy_batch_workspace_size) exceeds
+ * it fails with KVR_EUNSUPPORTED and enqueues nothing. Every call on one GPU
+ * shares that array: calls that overlap in time on one GPU (other streams,
+ * other host threads) race and may return wrong entropies; calls on one
+ * stream are ordered and safe. `stream` must belong to the current device
+ * (KVR_EINVAL otherwise). Nothing needs clearing between calls: every partial
+ * a call reads was written earlier in the same call.
+ */
+int kvr_logit_entropy_batch_noalloc(const kvr_logit_set *sets, int32_t nsets, hipStream_t stream);
 
 /*
  * kvr_logit_entropy_sample -- kvr_logit_entropy and the next token of every

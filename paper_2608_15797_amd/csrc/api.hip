@@ -377,6 +377,31 @@ int kvr_logit_entropy_batch(const kvr_logit_set *sets, int32_t nsets, void *work
   return hip_status(kvr::launch_logit_entropy_batch(b, stream), "kvr_logit_entropy_batch launch");
 }
 
+int kvr_logit_entropy_batch_noalloc(const kvr_logit_set *sets, int32_t nsets, hipStream_t stream) {
+  kvr::EntropyBatch b;
+  size_t need = 0;
+  int st = entropy_batch(sets, nsets, &b, &need);
+  if (st) return st;
+  if (need > kvr::kEntropyScratchBytes)
+    return fail(KVR_EUNSUPPORTED, "the split partials need %zu bytes, more than the %zu bytes of library scratch",
+                need, kvr::kEntropyScratchBytes);
+  if (need) {
+    int dev = -1, sdev = -1;
+    st = hip_status(hipGetDevice(&dev), "kvr_logit_entropy_batch_noalloc: hipGetDevice");
+    if (st) return st;
+    st = hip_status(hipStreamGetDevice(stream, &sdev), "kvr_logit_entropy_batch_noalloc: hipStreamGetDevice");
+    if (st) return st;
+    if (sdev != dev)
+      return fail(KVR_EINVAL, "stream belongs to device %d, the current device is %d", sdev, dev);
+    void *ws = nullptr;
+    st = hip_status(kvr::entropy_scratch(&ws), "kvr_logit_entropy_batch_noalloc: scratch address");
+    if (st) return st;
+    for (int k = 0; k < nsets; k++)
+      b.set[k].ws = static_cast<char *>(ws) + (size_t)b.row0[k] * b.set[k].splits * 4 * sizeof(float);
+  }
+  return hip_status(kvr::launch_logit_entropy_batch(b, stream), "kvr_logit_entropy_batch_noalloc launch");
+}
+
 size_t kvr_logit_entropy_sample_workspace_size(int32_t R, int32_t V, int32_t top_k) {
   if (R <= 0 || V <= 0 || top_k < 1 || top_k > kvr::kTopKMax) return 0;
   return kvr::sample_workspace_bytes(R, V, top_k);

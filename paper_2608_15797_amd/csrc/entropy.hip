@@ -37,10 +37,18 @@
 // key (seed, 0), top 24 bits of the first word).
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "kvr_device.h"
 #include "kvr_internal.h"
 
 namespace kvr {
+
+// Split partials of the allocation-free entropy entry point: one file-scope
+// device array per GPU, held until the process ends. Host code never uses
+// its name as an address; it uses the per-device pointer from
+// entropy_scratch() below.
+__device__ __align__(256) unsigned char scratch[kEntropyScratchBytes];
 
 namespace {
 
@@ -717,6 +725,26 @@ static hipError_t launch_partials(const EntropyBatch &b, bool sample, hipStream_
     else launch_split<bf16_t, false>(b, sample, rows, grid, stream);
   }
   return hipGetLastError();
+}
+
+hipError_t entropy_scratch(void **ptr) {
+  // Device address of `scratch` on the current device, looked up once per
+  // device with that device current (each GPU holds its own copy).
+  constexpr int kMaxDevices = 64;
+  static std::atomic<void *> cache[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void *p = cache[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    cache[dev].store(p, std::memory_order_release);
+  }
+  *ptr = p;
+  return hipSuccess;
 }
 
 hipError_t launch_logit_entropy_batch(const EntropyBatch &b, hipStream_t stream) {

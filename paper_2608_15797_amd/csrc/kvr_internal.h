@@ -119,6 +119,10 @@ size_t sample_workspace_bytes(int R, int V, int top_k);
 constexpr int kTopKMax = 64;
 hipError_t launch_logit_entropy(const EntropyParams &p, hipStream_t stream);
 hipError_t launch_logit_entropy_batch(const EntropyBatch &b, hipStream_t stream);
+// Library-held device scratch of kvr_logit_entropy_batch_noalloc (split
+// partials), per GPU; *ptr receives its address on the current device.
+constexpr size_t kEntropyScratchBytes = (size_t)1 << 20;
+hipError_t entropy_scratch(void **ptr);
 
 struct ForkParams {
   const void *sk, *sv;

@@ -26,7 +26,8 @@ EXPORTS = ("kvr_strerror", "kvr_last_error", "kvr_decode_attn", "kvr_decode_attn
            "kvr_accumulate_scores", "kvr_evict_topb", "kvr_logit_entropy",
            "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append",
            "kvr_logit_entropy_sample", "kvr_logit_entropy_sample_workspace_size",
-           "kvr_redundancy_scores", "kvr_logit_entropy_batch", "kvr_logit_entropy_batch_workspace_size")
+           "kvr_redundancy_scores", "kvr_logit_entropy_batch", "kvr_logit_entropy_batch_workspace_size",
+           "kvr_logit_entropy_batch_noalloc")
 
 
 class KvrError(RuntimeError):
@@ -95,6 +96,8 @@ def _load():
     lib.kvr_logit_entropy_batch.restype = ctypes.c_int
     lib.kvr_logit_entropy_batch_workspace_size.argtypes = [P(c_logit_set), i32]
     lib.kvr_logit_entropy_batch_workspace_size.restype = sz
+    lib.kvr_logit_entropy_batch_noalloc.argtypes = [P(c_logit_set), i32, vp]
+    lib.kvr_logit_entropy_batch_noalloc.restype = ctypes.c_int
     lib.kvr_logit_entropy_sample.argtypes = [vp, i32, i32, i32, i64, f32, vp, P(c_detector),
                                              P(c_sampler), vp, vp, sz, vp]
     lib.kvr_logit_entropy_sample.restype = ctypes.c_int
@@ -314,6 +317,17 @@ def logit_entropy_batch(sets, workspace: Optional[torch.Tensor] = None, stream=N
                                      0 if workspace is None else workspace.numel() * workspace.element_size(),
                                      _stream(stream))
     _check(rc, "kvr_logit_entropy_batch")
+
+
+ENTROPY_SCRATCH_BYTES = 1 << 20  # KVR_ENTROPY_SCRATCH_BYTES
+
+
+def logit_entropy_batch_noalloc(sets, stream=None) -> None:
+    """kvr_logit_entropy_batch_noalloc: as logit_entropy_batch, with the split
+    partials in the library's own device scratch (no workspace argument)."""
+    arr = _logit_sets(sets)
+    rc = lib.kvr_logit_entropy_batch_noalloc(arr, len(sets), _stream(stream))
+    _check(rc, "kvr_logit_entropy_batch_noalloc")
 
 
 def fork(src: Cache, dst: Cache, src_index: torch.Tensor, len_: torch.Tensor,

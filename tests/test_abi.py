@@ -196,3 +196,18 @@ def test_lds_limits_rejected_on_host():
     # Window recompute (bf16): cap words of LDS.
     c = _cache(kvr, cap=16385)
     assert kvr.lib.kvr_accumulate_scores(ctypes.byref(c), 16, 16, 8, 8, 1.0, 16, 0, None) == -2
+
+
+def test_entropy_noalloc_rejects_on_host():
+    """The allocation-free entropy call validates like the workspace call and
+    refuses, before any GPU work, a split plan larger than its scratch."""
+    from paper_2608_15797_amd import kvr
+    f = kvr.lib.kvr_logit_entropy_batch_noalloc
+    arr = (kvr.c_logit_set * 1)()
+    # 200 rows of 2^24 logits: 820 splits of 16-byte partials per row, 2.6 MB.
+    arr[0] = kvr.c_logit_set(16, 1, 200, 1 << 24, 1 << 24, 1.0, 16, None)
+    assert kvr.lib.kvr_logit_entropy_batch_workspace_size(arr, 1) > kvr.ENTROPY_SCRATCH_BYTES
+    assert f(arr, 1, None) == -2 and "scratch" in kvr.lib.kvr_last_error().decode()
+    assert f(None, 1, None) == -1
+    arr[0] = kvr.c_logit_set(16, 1, 4, 10, 5, 1.0, 16, None)
+    assert f(arr, 1, None) == -1
