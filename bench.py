@@ -28,14 +28,18 @@ prompt is decoded (teacher-forced) first; then the warmup steps, then exactly
 K timed steps between two synchronisations, with HIP events on the launch
 stream around each call of the dominant call (the roofline's kernel time).
 A replay of the same K step indices brackets every call with events for the
-per-call table. Unless the window already is one, a whole cycle is then timed
-the same way and reported under "cycle".
+per-call table. When the entropies ride in the base-attention launch, a second
+pass runs, at every step of the window, the fused call, base attention alone
+and the entropy call alone, one after the other, three times: the difference
+between the fused call and base attention alone is entropy's marginal time
+("entropy_marginal"). Unless the window already is one, a whole
+cycle is then timed and replayed the same way and reported under "cycle".
 
 Marker kernels (torch.cuda._sleep, a one-thread spin kernel) bracket every
 pass, so that a profile of this command can be cut into its passes (profsum
 --window): for each workload in order, marker before the timed pass, after
-it, after its replay, and, when a cycle is run, after the cycle's timed pass
-and after its replay.
+it, after its replay, after the entropy-marginal pass (when entropy is fused), and,
+when a cycle is run, after the cycle's timed pass and after its replay.
 
 One JSON line is printed.
 """
@@ -50,6 +54,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+from paper_2608_15797_amd import accounting as acc  # noqa: E402
 from paper_2608_15797_amd.benchplan import (PEAK_HBM_GBPS, Schedule, cycle_start, cycle_steps,  # noqa: E402
                                              dominant_call, place_window, step_bytes, window_bytes,
                                              window_stats)
@@ -116,6 +121,32 @@ def per_call(wl, dec, steps):
     return calls, moved_rows
 
 
+def entropy_marginal(wl, dec, steps, reps=3):
+    """Entropy's marginal time in the fused base-attention launch: for every
+    step of `steps`, the fused call, base attention alone and the entropy
+    call alone, one after the other, each between timing events, `reps`
+    times. marginal = mean(fused) - mean(alone)."""
+    import torch
+    timers = {}
+    for _ in range(reps):
+        for i in steps:
+            t = dec.T_prompt + i
+            si = dec.inputs(t)
+            dec.base_attn(t, si, timers=timers, sets=dec.logit_sets(si))
+            dec.base_attn(t, si, timers=timers)
+            dec.entropy(si, timers=timers)
+    torch.cuda.synchronize()
+    avg = {k: sum(s.elapsed_time(e) for s, e in ev) / len(ev) * 1e3 for k, ev in timers.items()}
+    eb = acc.entropy_bytes(wl)
+    mus = avg["base_attn_entropy"] - avg["base_attn"]
+    return dict(calls_per_kind=len(timers["base_attn"]), fused_call_us=round(avg["base_attn_entropy"], 2),
+                base_attn_alone_us=round(avg["base_attn"], 2), marginal_us=round(mus, 2),
+                separate_call_us=round(avg["entropy"], 2), bytes_per_step=eb,
+                GBps=round(eb / (mus * 1e-6) / 1e9, 1) if mus > 0 else None,
+                frac=round(eb / (mus * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4) if mus > 0 else None,
+                separate_frac=round(eb / (avg["entropy"] * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4))
+
+
 def summary(wl, dec, steps, ms, moved_rows):
     K = len(steps)
     tot = sum(window_bytes(wl, dec, steps, moved_rows).values())
@@ -158,11 +189,20 @@ def run_workload(name, K, W, instrument=True, cycle=True):
     marker()
     log("[%s] timed %d steps: %.4f ms/step" % (name, K, ms / K))
     calls, moved_rows = {}, None
+    marginal = None
     if instrument:
         calls, moved_rows = per_call(wl, dec, win)
         log("[%s] per-call: %s" % (name, json.dumps(calls)))
-    marker()
+        marker()
+        if dec.fuse_entropy:
+            marginal = entropy_marginal(wl, dec, win)
+            marker()
+            log("[%s] entropy marginal: %s" % (name, json.dumps(marginal)))
+    else:
+        marker()
     res = dict(workload=name, window=wstat, **summary(wl, dec, win, ms, moved_rows), calls=calls)
+    if marginal:
+        res["entropy_marginal"] = marginal
     # The dominant call's kernel time, from the events inside the timed pass.
     dur = [s.elapsed_time(e) for s, e in dom_ev]
     dom_steps = [i for i in win if dom in step_bytes(wl, dec, i)]

@@ -296,6 +296,28 @@ int kvr_logit_entropy_batch(const kvr_logit_set *sets, int32_t nsets, void *work
  * are not read); 0 when those are invalid. */
 size_t kvr_logit_entropy_batch_workspace_size(const kvr_logit_set *sets, int32_t nsets);
 
+/*
+ * kvr_decode_attn_entropy -- kvr_decode_attn over the sequences' own caches
+ * (no prefix) and kvr_logit_entropy_batch over the step's logit sets in one
+ * launch: the detector's entropies are by-products of the decode step (App.
+ * C: the signals add negligible cost), so their rows are read while the
+ * attention units stream their caches (Eq. (1) third line; Eq. (4)).
+ *
+ * Arguments, results and errors are those of kvr_decode_attn (with prefix =
+ * NULL and no workspace) and of kvr_logit_entropy_batch (sets, nsets), with
+ * one more requirement: every set's rows start 16-byte aligned (logits and
+ * ld * element size), KVR_EINVAL otherwise. Each logit row is reduced whole
+ * by one wavefront of the launch, so no workspace is needed. The attention
+ * outputs and scores are bit for bit those of kvr_decode_attn; the entropies
+ * agree with kvr_logit_entropy_batch to float32 rounding (different summation
+ * order). For a float32 cache the entropy rows run as a second kernel on the
+ * same stream.
+ */
+int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq, float scale,
+                            const void *k_new, const void *v_new, const int32_t *new_pos, void *out,
+                            const kvr_policy *policy, float *scores, const kvr_logit_set *sets, int32_t nsets,
+                            hipStream_t stream);
+
 /* Bytes of device scratch the library holds per GPU for
  * kvr_logit_entropy_batch_noalloc (the largest workspace it accepts). */
 #define KVR_ENTROPY_SCRATCH_BYTES ((size_t)1 << 20)

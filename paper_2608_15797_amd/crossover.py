@@ -67,7 +67,7 @@ def _qkv(S, L, Hq, Hkv, D, seed, tag):
 def evicted_ms(S, L, Hq, Hkv, D, B, W, buffer, reps=3, seed=7):
     """(amortised ms/step over an eviction cycle, scored step at B'+1, one
     eviction call, unscored step at B') for the evicted base path."""
-    cap = B + buffer + 1
+    cap = (B + buffer + 1 + 15) // 16 * 16  # heads 4 KiB-aligned, as the decode driver allocates
     cache = kvr.Cache.empty(S, L, Hkv, cap, D, torch.bfloat16)
     synth.fill_normal_(cache.k, 1.0, seed, "ev", "k")
     synth.fill_normal_(cache.v, 1.0, seed, "ev", "v")

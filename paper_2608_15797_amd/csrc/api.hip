@@ -87,10 +87,16 @@ size_t kvr_decode_attn_workspace_size(const kvr_cache *cache, const kvr_prefix *
   return kvr::attn_workspace_bytes(cache->S, cache->L, Hq, cache->D, ns);
 }
 
-int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len,
-                    const void *q, int32_t Hq, float scale, const void *k_new, const void *v_new,
-                    const int32_t *new_pos, void *out, const kvr_policy *policy, float *scores,
-                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Validates the arguments of kvr_decode_attn and fills p.
+int attn_params(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len, const void *q, int32_t Hq,
+                float scale, const void *k_new, const void *v_new, const int32_t *new_pos, void *out,
+                const kvr_policy *policy, float *scores, void *workspace, size_t workspace_bytes,
+                kvr::AttnParams *pp) {
+  kvr::AttnParams &p = *pp;
   int G = 0;
   int st = check_cache(cache, Hq, &G);
   if (st) return st;
@@ -103,7 +109,7 @@ int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int3
     return fail(KVR_EINVAL, "k_new/v_new not 16-byte aligned");
   if ((policy == nullptr) != (scores == nullptr))
     return fail(KVR_EINVAL, "policy and scores must both be given or both be NULL");
-  kvr::AttnParams p{};
+  p = kvr::AttnParams{};
   p.k = cache->k; p.v = cache->v; p.pos = cache->pos;
   p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.Hq = Hq; p.G = G;
   p.cap = cache->cap; p.D = cache->D; p.dtype = cache->dtype;
@@ -145,7 +151,22 @@ int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int3
     const size_t lds = ((size_t)G * p.D + (size_t)G * nt + 32) * sizeof(float);
     if (lds > 65536) return fail(KVR_EUNSUPPORTED, "float32 path needs %zu bytes of LDS (> 64 KiB)", lds);
   }
-  return hip_status(kvr::launch_decode_attn(p, stream), "kvr_decode_attn launch");
+  return KVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len,
+                    const void *q, int32_t Hq, float scale, const void *k_new, const void *v_new,
+                    const int32_t *new_pos, void *out, const kvr_policy *policy, float *scores,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  kvr::AttnParams p;
+  const int st = attn_params(cache, prefix, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores,
+                             workspace, workspace_bytes, &p);
+  if (st) return st;
+  return hip_status(kvr::launch_decode_attn(p, nullptr, stream), "kvr_decode_attn launch");
 }
 
 int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void *q_win,
@@ -430,6 +451,31 @@ int kvr_logit_entropy_sample(const void *logits, int32_t dtype, int32_t R, int32
   st = attach_workspace(&p, kvr::sample_workspace_bytes(R, V, sampler->top_k), workspace, workspace_bytes);
   if (st) return st;
   return hip_status(kvr::launch_logit_entropy(p, stream), "kvr_logit_entropy_sample launch");
+}
+
+}  // extern "C"
+
+extern "C" {
+
+int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq, float scale,
+                            const void *k_new, const void *v_new, const int32_t *new_pos, void *out,
+                            const kvr_policy *policy, float *scores, const kvr_logit_set *sets, int32_t nsets,
+                            hipStream_t stream) {
+  kvr::AttnParams p;
+  int st = attn_params(cache, nullptr, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, nullptr, 0,
+                       &p);
+  if (st) return st;
+  kvr::EntropyBatch b;
+  size_t need = 0;
+  st = entropy_batch(sets, nsets, &b, &need);
+  if (st) return st;
+  const size_t esz = sets[0].dtype == KVR_F32 ? 4 : 2;
+  for (int k = 0; k < nsets; k++)
+    if (!aligned16(sets[k].logits) || ((size_t)sets[k].ld * esz) % 16 != 0)
+      return fail(KVR_EINVAL, "set %d: logit rows must start 16-byte aligned (logits and ld * element size)", k);
+  if ((double)b.row0[nsets] + (double)cache->S * cache->L * cache->Hkv > 2147483647.0)
+    return fail(KVR_EUNSUPPORTED, "logit rows plus attention units exceed the launch grid");
+  return hip_status(kvr::launch_decode_attn(p, &b, stream), "kvr_decode_attn_entropy launch");
 }
 
 }  // extern "C"

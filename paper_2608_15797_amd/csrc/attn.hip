@@ -38,6 +38,7 @@
 
 #include <atomic>
 
+#include "entropy_common.h"
 #include "kvr_device.h"
 #include "kvr_internal.h"
 
@@ -46,7 +47,6 @@ namespace kvr {
 
 namespace {
 
-constexpr float kNegInf = -__builtin_huge_valf();
 
 template <int D>
 struct Geo {
@@ -212,6 +212,147 @@ __device__ __forceinline__ void stream_chunks(rsrc_t K, rsrc_t V, int k0, int k1
   }
 }
 
+// s_waitcnt vmcnt(N), other counters unconstrained (N < 64).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Evicted-cache chunks with the key rows in LDS: key rows are read as whole
+// rows (four 256-byte rows per 1 KiB instruction at D = 128) by buffer-to-LDS
+// loads into a ring slot, and the matrix-core operands are read back from
+// there. Loading the operand layout directly would take 64 bytes of each of 16
+// rows per instruction, which streams measurably slower from HBM. The 16-byte
+// units of a row are stored rotated by the row index (unit u of row r at
+// position u ^ (r mod units per row)), so the 16 lanes reading one unit of 16
+// consecutive rows hit distinct banks. Value rows stay in registers.
+template <int D>
+struct KLds {
+  static constexpr int ROW = D * 2;        // bytes per key row
+  static constexpr int RU = ROW / 16;      // 16-byte units per row
+  static constexpr int RPI = 1024 / ROW;   // rows per buffer-to-LDS instruction
+};
+
+template <int D, int TILES>
+struct VChunk {
+  uint32_t v[TILES][4][Geo<D>::VW];
+};
+
+// Per-lane byte offsets of the loads of one chunk, relative to the chunk's
+// first row; they do not change from chunk to chunk (the chunk's base goes
+// into the buffer resource), so the stream loop does no vector address
+// arithmetic. Key load I covers rows RPI*I .. RPI*I + RPI - 1: lane l writes
+// LDS unit l of the load, which holds row RPI*I + l / RU, unit
+// (l % RU) ^ (row % RU). Value loads: row 16t + 4 g4 + cc at byte 16 r16 *
+// (D / 128), the cc rows apart by ROW bytes (the instruction offset).
+template <int D, int TILES>
+struct KLOffsets {
+  static constexpr int KI = 16 * TILES * KLds<D>::ROW / 1024;
+  uint32_t k[KI];
+  uint32_t v[TILES];
+  __device__ __forceinline__ explicit KLOffsets(int lane) {
+#pragma unroll
+    for (int I = 0; I < KI; I++) {
+      const int row = KLds<D>::RPI * I + lane / KLds<D>::RU;
+      const int u = (lane % KLds<D>::RU) ^ (row % KLds<D>::RU);
+      k[I] = (uint32_t)row * KLds<D>::ROW + (uint32_t)u * 16u;
+    }
+    const int r16 = lane & 15, g4 = lane >> 4;
+#pragma unroll
+    for (int t = 0; t < TILES; t++) v[t] = (uint32_t)(t * 16 + 4 * g4) * (D * 2) + (uint32_t)r16 * (Geo<D>::NB * 2);
+  }
+};
+
+// Loads of one chunk of 16*TILES keys starting at row c0 of the unit's K and
+// V (kbase, vbase) with `rows` rows readable from kbase/vbase (loads past them
+// return zero): the key rows into `slot` (LDS), then the value rows into
+// registers. Issues KI + 4 * TILES vector-memory instructions.
+template <int D, int TILES>
+__device__ __forceinline__ void load_chunk_lds(VChunk<D, TILES> &c, char *slot, const bf16_t *kbase, const bf16_t *vbase,
+                                               int rows, int c0, const KLOffsets<D, TILES> &off) {
+  constexpr uint32_t ROW = D * 2;
+  const uint32_t bytes = rows > c0 ? (uint32_t)(rows - c0) * ROW : 0u;
+  const rsrc_t K = make_rsrc(kbase + (size_t)c0 * D, bytes);
+  const rsrc_t V = make_rsrc(vbase + (size_t)c0 * D, bytes);
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+  for (int I = 0; I < KLOffsets<D, TILES>::KI; I++)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(K, (lds_void_t *)(slot + I * 1024), 16, off.k[I], 0, 0, 0);
+#endif
+#pragma unroll
+  for (int t = 0; t < TILES; t++)
+#pragma unroll
+    for (int cc = 0; cc < 4; cc++) {
+      if constexpr (D == 128) {
+        const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(V, off.v[t] + cc * ROW, 0, kStreamLoad);
+        c.v[t][cc][0] = x.x; c.v[t][cc][1] = x.y; c.v[t][cc][2] = x.z; c.v[t][cc][3] = x.w;
+      } else {
+        const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(V, off.v[t] + cc * ROW, 0, kStreamLoad);
+        c.v[t][cc][0] = x.x; c.v[t][cc][1] = x.y;
+      }
+    }
+}
+
+// Logits (log2 domain) of one LDS-resident chunk for one 16-row block, as
+// chunk_logits: key row 16t + r16, operand unit 4i + g4 (d = 32i + 8 g4).
+template <int D, int TILES>
+__device__ __forceinline__ void chunk_logits_lds(const char *slot, const short4_t (&qop)[Geo<D>::NB],
+                                                 float (&x)[TILES][4], int c0, int nlim, int r16, int g4,
+                                                 float sl2, bool tail) {
+#pragma unroll
+  for (int t = 0; t < TILES; t++) {
+    const int row = t * 16 + r16;
+    float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < Geo<D>::NLD; i++) {
+      const int u = (4 * i + g4) ^ (row % KLds<D>::RU);
+      const u32x4 kk = *reinterpret_cast<const u32x4 *>(slot + row * KLds<D>::ROW + u * 16);
+      acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(s4(kk.x, kk.y), qop[2 * i], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(s4(kk.z, kk.w), qop[2 * i + 1], acc, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) x[t][i] = acc[i] * sl2;
+    if (tail) {
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int key = c0 + t * 16 + 4 * g4 + i;
+        x[t][i] = key < nlim ? x[t][i] : kNegInf;
+      }
+    }
+  }
+}
+
+// stream_chunks_from for LDS-resident key rows: chunk c (from k0) sits in
+// ring slot c % DEPTH (slots of 16*TILES*2D bytes from `ring`) and value
+// register buffer c % DEPTH; buffer 0 / slot 0 already hold (or are loading)
+// the chunk at k0. Keys [k0, k1) of kbase / vbase are read. Before a chunk is
+// processed the wave waits until only the loads of the chunks after it are in
+// flight: nothing else is issued inside the loop, so that count is exact.
+template <int D, int TILES, int DEPTH, typename Pre, typename Proc>
+__device__ __forceinline__ void stream_chunks_lds(VChunk<D, TILES> (&buf)[DEPTH], char *ring, const bf16_t *kbase,
+                                                  const bf16_t *vbase, int k0, int k1,
+                                                  const KLOffsets<D, TILES> &off, Pre pre, Proc proc) {
+  constexpr int stride = 16 * TILES;
+  constexpr int SLOT = 16 * TILES * KLds<D>::ROW;
+  constexpr int PER = KLOffsets<D, TILES>::KI + 4 * TILES;  // instructions per chunk
+#pragma unroll
+  for (int s = 1; s < DEPTH - 1; s++)
+    load_chunk_lds<D, TILES>(buf[s], ring + s * SLOT, kbase, vbase, k1, k0 + s * stride, off);
+  pre();
+  for (int c0 = k0; c0 < k1; c0 += DEPTH * stride) {
+#pragma unroll
+    for (int j = 0; j < DEPTH; j++) {
+      const int cj = c0 + j * stride;
+      if (cj >= k1) break;
+      const int nb = (j + DEPTH - 1) % DEPTH;
+      load_chunk_lds<D, TILES>(buf[nb], ring + nb * SLOT, kbase, vbase, k1, cj + (DEPTH - 1) * stride, off);
+      wait_vm<PER * (DEPTH - 1)>();
+      proc(buf[j], ring + j * SLOT, cj);
+    }
+  }
+}
+
 // B operands of P.V for every instance b of every tile, from the four V rows
 // (keys 4*g4 + c, c = 0..3) each lane holds: operand b packs element b of
 // the four rows. Built once per chunk and shared by all row blocks.
@@ -322,16 +463,47 @@ __device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st, f
 // next chunk's loads are in flight while the current one is computed; the
 // appended token (slot n-1) is a final one-key tile read from k_new/v_new.
 constexpr size_t kBaseLdsFloor = 26 * 1024;  // see the evicted-cache launch
+constexpr size_t kMaxLds = 64 * 1024;        // LDS a workgroup may ask for
 constexpr int kFastPieces = 4;  // split partials per row merged with batched LDS reads
 
-template <int D, bool MERGE, int TILES, int DEPTH>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void attn_cache_bf16(AttnParams p) {
+// KL (evicted cache only): key rows through an LDS ring (load_chunk_lds)
+// instead of registers; the ring takes the first kl_ring<D, TILES, DEPTH>
+// bytes of LDS.
+template <int D, int TILES, int DEPTH>
+constexpr size_t kl_ring = (size_t)DEPTH * 16 * TILES * D * 2;
+// Chunk shape of the evicted-cache launch with LDS key rows.
+constexpr int kKlTiles = 2;
+constexpr int kKlDepth = 2;
+
+// LT (evicted cache only): 0, or the logit type of the step's entropy rows
+// computed in the same launch (1 = bfloat16, 2 = float32). The first
+// e.row0[e.nsets] workgroups of the grid are then one wave per logit row
+// (entropy_row_wave: the whole row, its entropy and detector update, no
+// partials); they are dispatched first and stream their rows while the
+// attention units run. The other workgroups are the attention units.
+template <int D, bool MERGE, int TILES, int DEPTH, bool KL = false, int LT = 0>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void attn_cache_bf16(AttnParams p,
+                                                                                               EntropyBatch e) {
+  static_assert(!(KL && MERGE), "LDS key rows are for the evicted cache");
+  static_assert(!(LT && MERGE), "entropy rows ride with the evicted cache");
   constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
   constexpr uint32_t ROW = D * 2;
   extern __shared__ float smem[];
 
-  const int unit = blockIdx.x;  // ((s * L) + l) * Hkv + h
+  int unit = blockIdx.x;  // ((s * L) + l) * Hkv + h
+  if constexpr (LT != 0) {
+    const int rows = e.row0[e.nsets];
+    if (unit < rows) {
+      const int k = batch_set(e, unit);
+      if constexpr (LT == 1)
+        entropy_row_wave<bf16_t, 12>(e.set[k], unit - e.row0[k], threadIdx.x);
+      else
+        entropy_row_wave<float, 6>(e.set[k], unit - e.row0[k], threadIdx.x);
+      return;
+    }
+    unit -= rows;
+  }
   const int h = unit % p.Hkv;
   const int sl = unit / p.Hkv;
   const int l = sl % p.L;
@@ -362,10 +534,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
   load_qop<D>(r16 < G ? static_cast<const bf16_t *>(p.q) + (qrow0 + r16) * D : nullptr, g4, qop);
   KVChunk<D, 1> cn;
   if (kn) load_chunk<D, 1>(cn, make_rsrc(kn, ROW), make_rsrc(vn, ROW), 0, r16, g4);
-  KVChunk<D, TILES> ring[DEPTH];
+  KVChunk<D, TILES> ring[KL ? 1 : DEPTH];
+  VChunk<D, TILES> vring[KL ? DEPTH : 1];
+  char *kring = reinterpret_cast<char *>(smem);  // KL: [DEPTH][CH rows of ROW bytes]
+  const KLOffsets<D, TILES> kloff(lane);
   if constexpr (!MERGE) {
-    const uint32_t first = (uint32_t)(p.cap < CH ? p.cap : CH) * ROW;
-    load_chunk<D, TILES>(ring[0], make_rsrc(Kc, first), make_rsrc(Vc, first), 0, r16, g4);
+    const int first = p.cap < CH ? p.cap : CH;
+    if constexpr (KL)
+      load_chunk_lds<D, TILES>(vring[0], kring, Kc, Vc, first, 0, kloff);
+    else
+      load_chunk<D, TILES>(ring[0], make_rsrc(Kc, (uint32_t)first * ROW), make_rsrc(Vc, (uint32_t)first * ROW), 0,
+                           r16, g4);
   }
 
   int n = p.len[s];
@@ -406,8 +585,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
   const int wstart = p.B + p.buffer + 2 - p.W;
   const bool win = !MERGE && p.scores != nullptr && n >= wstart;
   const int ldx = (p.cap + 63) & ~63;
-  float *xs = smem;                 // [G][ldx] logits of window steps
-  float *stat = smem + G * ldx;     // [16] max, [16] 1/sum
+  float *xs = smem + (KL ? kl_ring<D, TILES, DEPTH> / sizeof(float) : 0);  // [G][ldx] logits of window steps
+  float *stat = xs + G * ldx;       // [16] max, [16] 1/sum
 
   const float sl2 = p.scale * kLog2e;
   RowState st{kNegInf, 0.0f};
@@ -417,7 +596,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
 
   const rsrc_t Kr = make_rsrc(Kc, (uint32_t)ncache * ROW);
   const rsrc_t Vr = make_rsrc(Vc, (uint32_t)ncache * ROW);
-  auto process = [&](KVChunk<D, TILES> &c, int c0, int nlim) {
+  // One chunk: c holds the value rows (and, without KL, the key rows); with
+  // KL the key rows are in the LDS slot `kslot`.
+  auto process = [&](auto &c, const char *kslot, int c0, int nlim) {
     if (!MERGE && c0 == 0 && nlim < CH) {
       // The first chunk was read before the live length was known.
 #pragma unroll
@@ -429,7 +610,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
             for (int w = 0; w < Geo<D>::VW; w++) c.v[t][cc][w] = 0u;
     }
     float x[TILES][4];
-    chunk_logits<D, TILES>(c, qop, x, c0, nlim, g4, sl2, c0 + CH > nlim);
+    if constexpr (KL)
+      chunk_logits_lds<D, TILES>(kslot, qop, x, c0, nlim, r16, g4, sl2, c0 + CH > nlim);
+    else
+      chunk_logits<D, TILES>(c, qop, x, c0, nlim, g4, sl2, c0 + CH > nlim);
     if (win && r16 < G) {
 #pragma unroll
       for (int t = 0; t < TILES; t++)
@@ -478,8 +662,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
     }
   };
   if constexpr (MERGE) load_chunk<D, TILES>(ring[0], Kr, Vr, 0, r16, g4);
-  stream_chunks_from<D, TILES, DEPTH>(ring, Kr, Vr, 0, ncache, r16, g4, new_token,
-                                      [&](KVChunk<D, TILES> &c, int c0) { process(c, c0, ncache); });
+  if constexpr (KL)
+    stream_chunks_lds<D, TILES, DEPTH>(vring, kring, Kc, Vc, 0, ncache, kloff, new_token,
+                                       [&](VChunk<D, TILES> &c, const char *slot, int c0) { process(c, slot, c0, ncache); });
+  else
+    stream_chunks_from<D, TILES, DEPTH>(ring, Kr, Vr, 0, ncache, r16, g4, new_token,
+                                        [&](KVChunk<D, TILES> &c, int c0) { process(c, nullptr, c0, ncache); });
+#if defined(__HIP_DEVICE_COMPILE__)
+  if constexpr (KL) __builtin_amdgcn_s_waitcnt(0);  // no buffer-to-LDS load outlives the stream
+#endif
   if (append && win && r16 < G && g4 == 0) xs[r16 * ldx + n - 1] = xnew;
 
   float z = st.zl;
@@ -866,8 +1057,23 @@ size_t prefix_lds_bytes(int rb) {
   return (size_t)rb * 16 * kRecFloats<D> * sizeof(float);
 }
 
+// The evicted-cache kernel with the entropy rows of `e` (nullptr: none) in
+// front of its units.
+template <int D, int TILES, int DEPTH, bool KL>
+void launch_own(const AttnParams &p, const EntropyBatch *e, size_t lds, hipStream_t stream) {
+  const int rows = e ? e->row0[e->nsets] : 0;
+  const dim3 grid(rows + p.S * p.L * p.Hkv);
+  const EntropyBatch none{};
+  if (!e)
+    hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 0>), grid, dim3(64), lds, stream, p, none);
+  else if (e->set[0].dtype == 0)
+    hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 2>), grid, dim3(64), lds, stream, p, *e);
+  else
+    hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 1>), grid, dim3(64), lds, stream, p, *e);
+}
+
 template <int D>
-hipError_t launch_bf16(const AttnParams &p_in, hipStream_t stream) {
+hipError_t launch_bf16(const AttnParams &p_in, const EntropyBatch *ent, hipStream_t stream) {
   AttnParams p = p_in;
   if (p.P > 0) {
     // LDS for the suffix kernel's prefetched partials: whole 1 KiB blocks per
@@ -882,9 +1088,16 @@ hipError_t launch_bf16(const AttnParams &p_in, hipStream_t stream) {
     // 6 single-wave workgroups per CU (160 KiB) instead of the 8 its registers
     // allow: fewer concurrent short K/V streams measured 2.5-3.5% faster
     // (5 per CU lost at short caches, 7 matched 6).
-    const size_t need = p.scores ? ((size_t)p.G * ((p.cap + 63) & ~63) + 32) * sizeof(float) : 0;
+    const size_t logits = p.scores ? ((size_t)p.G * ((p.cap + 63) & ~63) + 32) * sizeof(float) : 0;
     const size_t lds_min = D == 128 ? kBaseLdsFloor : 0;
-    hipLaunchKernelGGL((attn_cache_bf16<D, false, 2, 2>), units, dim3(64), need > lds_min ? need : lds_min, stream, p);
+    constexpr size_t ring = kl_ring<D, kKlTiles, kKlDepth>;
+    if (ring + logits <= kMaxLds) {
+      // Key rows through the LDS ring.
+      const size_t need = ring + logits;
+      launch_own<D, kKlTiles, kKlDepth, true>(p, ent, need > lds_min ? need : lds_min, stream);
+    } else {
+      launch_own<D, 2, 2, false>(p, ent, logits > lds_min ? logits : lds_min, stream);
+    }
     return hipGetLastError();
   }
   // Context splits first; the suffix kernel then merges their partials.
@@ -901,8 +1114,17 @@ hipError_t launch_bf16(const AttnParams &p_in, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_cache_bf16<D, true, 2, 2>), units, dim3(64),
-                     (size_t)p.merge_pf * p.merge_blk * sizeof(float), stream, p);
+                     (size_t)p.merge_pf * p.merge_blk * sizeof(float), stream, p, EntropyBatch{});
   return hipGetLastError();
+}
+
+// Whole logit rows, one wave per row, as a kernel of its own (the entropy
+// rows of a float32-cache launch, whose attention kernel has no such lanes).
+template <typename T>
+__global__ __launch_bounds__(64) void entropy_rows_kernel(EntropyBatch e) {
+  const int g = blockIdx.x;
+  const int k = batch_set(e, g);
+  entropy_row_wave<T, sizeof(T) == 2 ? 12 : 6>(e.set[k], g - e.row0[k], threadIdx.x);
 }
 
 }  // namespace
@@ -967,14 +1189,20 @@ size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit) {
   return (size_t)nsplit * S * L * Hq * (D == 128 ? kRecFloats<128> : kRecFloats<64>) * sizeof(float);
 }
 
-hipError_t launch_decode_attn(const AttnParams &p, hipStream_t stream) {
+hipError_t launch_decode_attn(const AttnParams &p, const EntropyBatch *ent, hipStream_t stream) {
   if (p.dtype == 0) {
     const int nt_max = (p.P > 0 ? p.plen : 0) + p.cap;
     const size_t lds = f32_attn_lds_bytes(p.G, p.D, p.P > 0 ? p.plen : 0, p.cap);
     hipLaunchKernelGGL(attn_f32, dim3(p.S * p.L * p.Hkv), dim3(64), lds, stream, p, nt_max);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !ent) return e;
+    const dim3 rows(ent->row0[ent->nsets]);
+    if (ent->set[0].dtype == 0) hipLaunchKernelGGL(entropy_rows_kernel<float>, rows, dim3(64), 0, stream, *ent);
+    else hipLaunchKernelGGL(entropy_rows_kernel<bf16_t>, rows, dim3(64), 0, stream, *ent);
     return hipGetLastError();
   }
-  return p.D == 128 ? launch_bf16<128>(p, stream) : launch_bf16<64>(p, stream);
+  if (ent && p.P > 0) return hipErrorInvalidValue;
+  return p.D == 128 ? launch_bf16<128>(p, ent, stream) : launch_bf16<64>(p, ent, stream);
 }
 
 }  // namespace kvr

@@ -39,6 +39,7 @@
 
 #include <atomic>
 
+#include "entropy_common.h"
 #include "kvr_device.h"
 #include "kvr_internal.h"
 
@@ -62,149 +63,6 @@ constexpr int kRoundVecs = kU * kThreads;   // vectors per workgroup per round
 constexpr int kRowThreads = 1024;
 constexpr int kRowMinRows = 256;
 constexpr int kRowMinVecs = 8 * kRowThreads;
-constexpr float kNegInf = -__builtin_huge_valf();
-
-struct Tri {
-  float m, z, s;
-};
-
-__device__ __forceinline__ Tri tri_merge(Tri a, Tri b) {
-  const float M = fmaxf(a.m, b.m);
-  if (M == kNegInf) return Tri{kNegInf, 0.f, 0.f};
-  Tri r{M, 0.f, 0.f};
-  if (a.z > 0.f) {
-    const float f = fast_exp2(a.m - M);
-    r.z += a.z * f;
-    r.s += (a.s + (a.m - M) * a.z) * f;
-  }
-  if (b.z > 0.f) {
-    const float f = fast_exp2(b.m - M);
-    r.z += b.z * f;
-    r.s += (b.s + (b.m - M) * b.z) * f;
-  }
-  return r;
-}
-
-// Fold a group of already scaled values (log2 domain) into the triple.
-template <int N>
-__device__ __forceinline__ void tri_add(Tri &t, const float (&y)[N]) {
-  float lm = y[0];
-#pragma unroll
-  for (int e = 1; e < N; e++) lm = fmaxf(lm, y[e]);
-  if (lm > t.m) {
-    if (t.z > 0.f) {
-      const float f = fast_exp2(t.m - lm);
-      t.s = (t.s + (t.m - lm) * t.z) * f;
-      t.z *= f;
-    }
-    t.m = lm;
-  }
-#pragma unroll
-  for (int e = 0; e < N; e++) {
-    // Clamp keeps (-inf) - m and (-inf) - (-inf) finite so 0 * d stays 0.
-    const float d = fmaxf(y[e] - t.m, -256.0f);
-    const float w = fast_exp2(d);
-    t.z += w;
-    t.s = fmaf(d, w, t.s);
-  }
-}
-
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ rsrc_t row_rsrc(const void *p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
-}
-
-// Eight logits of a row, held as the raw loaded words until they are used, so
-// that a round's loads cost 4 (bf16) or 8 (fp32) registers per vector.
-template <typename T>
-struct Vec8;
-template <>
-struct Vec8<bf16_t> {
-  u32x4 w;
-  __device__ __forceinline__ void load(rsrc_t r, int v) {
-    w = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 16u, 0, kStreamLoad);
-  }
-  __device__ __forceinline__ void get(float (&y)[8]) const {
-    y[0] = bf16_lo(w.x); y[1] = bf16_hi(w.x); y[2] = bf16_lo(w.y); y[3] = bf16_hi(w.y);
-    y[4] = bf16_lo(w.z); y[5] = bf16_hi(w.z); y[6] = bf16_lo(w.w); y[7] = bf16_hi(w.w);
-  }
-};
-template <>
-struct Vec8<float> {
-  u32x4 a, b;
-  __device__ __forceinline__ void load(rsrc_t r, int v) {
-    a = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u, 0, kStreamLoad);
-    b = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)v * 32u + 16u, 0, kStreamLoad);
-  }
-  __device__ __forceinline__ void get(float (&y)[8]) const {
-    y[0] = __uint_as_float(a.x); y[1] = __uint_as_float(a.y); y[2] = __uint_as_float(a.z); y[3] = __uint_as_float(a.w);
-    y[4] = __uint_as_float(b.x); y[5] = __uint_as_float(b.y); y[6] = __uint_as_float(b.z); y[7] = __uint_as_float(b.w);
-  }
-};
-
-// The triple's reference m may trail the running maximum by up to this much
-// (log2 units, a factor of 256): every term 2^(y - m) stays finite and exact
-// to fp32 rounding, and the rescale is skipped for almost every vector once
-// the first few have been seen. The entropy does not depend on m.
-constexpr float kSlack = 8.0f;
-
-__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
-
-// Fold eight raw logits x into the triple, y = c * x with c > 0.
-__device__ __forceinline__ void tri_fold8(Tri &t, const float (&x)[8], float c) {
-  // NaN-propagating maximum: no operand canonicalisation, three-input
-  // instructions (NaN logits are unsupported anyway).
-  const float lm = vmax(vmax(vmax(x[0], x[1]), vmax(x[2], x[3])), vmax(vmax(x[4], x[5]), vmax(x[6], x[7]))) * c;
-  if (lm > t.m + kSlack) {
-    if (t.z > 0.f) {
-      const float f = fast_exp2(t.m - lm);
-      t.s = (t.s + (t.m - lm) * t.z) * f;
-      t.z *= f;
-    }
-    t.m = lm;
-  }
-  const float nm = -t.m;
-#pragma unroll
-  for (int e = 0; e < 8; e++) {
-    // Clamp keeps -inf logits (and -inf - (-inf)) finite so 0 * d stays 0.
-    const float d = fmaxf(fmaf(x[e], c, nm), -256.0f);
-    const float w = fast_exp2(d);
-    t.z += w;
-    t.s = fmaf(d, w, t.s);
-  }
-}
-
-__device__ __forceinline__ float load1(const bf16_t *ptr) { return bf16_to_f32(*ptr); }
-__device__ __forceinline__ float load1(const float *ptr) { return *ptr; }
-
-__device__ __forceinline__ float finish_entropy(Tri t) {
-  return kLn2 * (log2f(t.z) - t.s / t.z);
-}
-
-// Detector update of one row by one whole wave (every lane passes the same
-// H): the history entries are read by the lanes in parallel, the new entry
-// taking its slot in registers, and summed with a wave reduction.
-__device__ void detector_push(const EntropyParams &p, int row, float H, int lane) {
-  if (!p.hist) return;
-  float *h = p.hist + (size_t)row * p.window;
-  const int c = p.cnt[row];
-  const int slot = c % p.window;
-  const int c1 = c + 1;
-  const int k = c1 < p.window ? c1 : p.window;
-  const bool judge = c1 >= p.guard;
-  float sum = 0.f;
-  if (judge) {
-    for (int i = lane; i < k; i += kWave) sum += i == slot ? H : h[i];
-    sum = wave_sum(sum);
-  }
-  if (lane == 0) {
-    h[slot] = H;
-    p.cnt[row] = c1;
-    if (judge && sum / (float)k > p.tau) p.flag[row] = 1;
-  }
-}
 
 // ---------------------------------------------------------------- sampler
 
@@ -388,15 +246,6 @@ __device__ __forceinline__ int gather_select(const uint64_t *cand, const int (&o
   }
   const uint64_t thr = select_threshold<NPL>(v, k, k);
   return wave_store_ge<NPL>(out, v, thr, lane);
-}
-
-// The set of a batch that holds global row g (uniform per workgroup).
-__device__ __forceinline__ int batch_set(const EntropyBatch &b, int g) {
-  int k = 0;
-#pragma unroll
-  for (int i = 1; i < kEntropyMaxSets; i++)
-    if (i < b.nsets && g >= b.row0[i]) k = i;
-  return k;
 }
 
 // One workgroup of NT threads per (split, global row of the batch).

@@ -44,7 +44,10 @@ void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int *n
                         int *nwaves);
 size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit);
 
-hipError_t launch_decode_attn(const AttnParams &p, hipStream_t stream);
+struct EntropyBatch;
+// ent: NULL, or the entropy rows computed in the same launch (own cache
+// only, no prefix; rows 16-byte aligned, no workspace).
+hipError_t launch_decode_attn(const AttnParams &p, const EntropyBatch *ent, hipStream_t stream);
 
 struct ScoreParams {
   const void *k, *v;

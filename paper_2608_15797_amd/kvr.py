@@ -27,7 +27,7 @@ EXPORTS = ("kvr_strerror", "kvr_last_error", "kvr_decode_attn", "kvr_decode_attn
            "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append",
            "kvr_logit_entropy_sample", "kvr_logit_entropy_sample_workspace_size",
            "kvr_redundancy_scores", "kvr_logit_entropy_batch", "kvr_logit_entropy_batch_workspace_size",
-           "kvr_logit_entropy_batch_noalloc")
+           "kvr_logit_entropy_batch_noalloc", "kvr_decode_attn_entropy")
 
 
 class KvrError(RuntimeError):
@@ -96,6 +96,9 @@ def _load():
     lib.kvr_logit_entropy_batch.restype = ctypes.c_int
     lib.kvr_logit_entropy_batch_workspace_size.argtypes = [P(c_logit_set), i32]
     lib.kvr_logit_entropy_batch_workspace_size.restype = sz
+    lib.kvr_decode_attn_entropy.argtypes = [P(c_cache), vp, vp, i32, f32, vp, vp, vp, vp, P(c_policy), vp,
+                                            P(c_logit_set), i32, vp]
+    lib.kvr_decode_attn_entropy.restype = ctypes.c_int
     lib.kvr_logit_entropy_batch_noalloc.argtypes = [P(c_logit_set), i32, vp]
     lib.kvr_logit_entropy_batch_noalloc.restype = ctypes.c_int
     lib.kvr_logit_entropy_sample.argtypes = [vp, i32, i32, i32, i64, f32, vp, P(c_detector),
@@ -236,6 +239,23 @@ def decode_attn(cache: Cache, len_: torch.Tensor, q: torch.Tensor, out: torch.Te
                              0 if workspace is None else workspace.numel() * workspace.element_size(),
                              _stream(stream))
     _check(rc, "kvr_decode_attn")
+
+
+def decode_attn_entropy(cache: Cache, len_: torch.Tensor, q: torch.Tensor, out: torch.Tensor, scale: float,
+                        sets, k_new=None, v_new=None, new_pos=None, policy: Optional[Policy] = None,
+                        scores: Optional[torch.Tensor] = None, stream=None) -> None:
+    """kvr_decode_attn_entropy: decode_attn over the own caches plus the
+    entropies of the LogitSet list `sets` in the same launch."""
+    cc = cache.c()
+    pol = policy.c() if policy is not None else None
+    for t in (len_, q, out, k_new, v_new, new_pos, scores):
+        assert t is None or t.is_contiguous()
+    arr = _logit_sets(sets)
+    rc = lib.kvr_decode_attn_entropy(ctypes.byref(cc), _ptr(len_), _ptr(q), q.shape[2], float(scale),
+                                     _ptr(k_new), _ptr(v_new), _ptr(new_pos), _ptr(out),
+                                     ctypes.byref(pol) if pol else None, _ptr(scores), arr, len(sets),
+                                     _stream(stream))
+    _check(rc, "kvr_decode_attn_entropy")
 
 
 def accumulate_scores(cache: Cache, len_: torch.Tensor, q_win: torch.Tensor, scale: float,

@@ -46,7 +46,7 @@ def run(workload: str = "base7b_helper", reps: int = 200, seed: int = 11, base=N
     if b is None:
         raise SystemExit("%s has no base model" % workload)
     dt = torch.bfloat16
-    S, L, Hq, Hkv, D, cap = b.S, b.L, b.Hq, b.Hkv, b.D, b.cap
+    S, L, Hq, Hkv, D, cap = b.S, b.L, b.Hq, b.Hkv, b.D, b.cache_cap
     n = b.B + (b.buffer + 2) // 2
     dev = "cuda"
     K = torch.empty((S, L, Hkv, cap, D), dtype=dt, device=dev)

@@ -7,9 +7,11 @@ helper candidates of every problem decode together) is:
   2. base:   kvr_evict_topb when the live length exceeds B + buffer;
   3. helper: kvr_decode_attn over the shared or private full context plus the
              candidate's own suffix (Sec. 3.1);
-  4. kvr_logit_entropy_batch over the logit rows of both models in one
-             launch, with the moving-average detector on the base rows
-             (Eq. (4); only base candidates are screened).
+  4. the entropies of the logit rows of both models, with the
+             moving-average detector on the base rows (Eq. (4); only base
+             candidates are screened): computed in the base-attention launch
+             of step 1 (kvr_decode_attn_entropy) when the workload has a base
+             model, else by one kvr_logit_entropy_batch call.
 
 All candidates advance in lockstep, so every live length is known on the host
 in advance: the driver precomputes per-token length tables on the device
@@ -78,10 +80,10 @@ class Decoder:
         dev = self.device
 
         if b:
-            self.bcache = kvr.Cache.empty(b.S, b.L, b.Hkv, b.cap, b.D, self.dt, dev)
+            self.bcache = kvr.Cache.empty(b.S, b.L, b.Hkv, b.cache_cap, b.D, self.dt, dev)
             self.bcache.k.zero_()
             self.bcache.v.zero_()
-            self.scores = torch.zeros((b.S, b.L, b.Hkv, b.cap), dtype=torch.float32, device=dev)
+            self.scores = torch.zeros((b.S, b.L, b.Hkv, b.cache_cap), dtype=torch.float32, device=dev)
             self.bout = torch.empty((b.S, b.L, b.Hq, b.D), dtype=self.dt, device=dev)
             self.policy = kvr.Policy(b.B, b.W, b.buffer)
             self.bscale = 1.0 / math.sqrt(b.D)
@@ -105,6 +107,8 @@ class Decoder:
             wsb = kvr.decode_attn_workspace_size(self.hcache, self.prefix if with_helper_prefix else None,
                                                  h.Hq)
             self.hws = torch.empty(max(wsb, 16) // 4 + 4, dtype=torch.float32, device=dev)
+        # Entropies ride in the base-attention launch when there is one.
+        self.fuse_entropy = bool(b and wl.logits)
         self.H = []
         self.ews = []
         for ls in wl.logits:
@@ -159,18 +163,16 @@ class Decoder:
 
     # -- one token ------------------------------------------------------------
     def base_token(self, t: int, si: StepInputs, stream=None, on_scored=None,
-                   timers=None, evict_log=None, only=None) -> bool:
+                   timers=None, evict_log=None, only=None, sets=None) -> bool:
         """Append + attend (+ score) for token t; evict if the cache overflows.
         Returns True when an eviction ran. `on_scored(t)` (tests) runs between
         the attention and the eviction. With `evict_log` (a list), each
         eviction appends the number of kept rows, over all heads, that changed
         slot (read back from the kept sets: a synchronising copy, for
-        accounting outside timed regions)."""
+        accounting outside timed regions). With `sets` (LogitSet list) the
+        entropies of those rows are computed in the same launch."""
         b = self.wl.base
-        with _timer(timers, "base_attn", stream, only):
-            kvr.decode_attn(self.bcache, self.blen[t], si.bq, self.bout, self.bscale,
-                            k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,
-                            scores=self.scores, stream=stream)
+        self.base_attn(t, si, stream, timers=timers, only=only, sets=sets)
         if on_scored is not None:
             on_scored(t)
         if self.blen_host[t] > b.B + b.buffer:
@@ -183,6 +185,20 @@ class Decoder:
             return True
         return False
 
+    def base_attn(self, t: int, si: StepInputs, stream=None, timers=None, only=None, sets=None) -> None:
+        """The base-attention call of token t alone (append, attend, score),
+        with the entropies of `sets` in the same launch when given."""
+        if sets:
+            with _timer(timers, "base_attn_entropy", stream, only):
+                kvr.decode_attn_entropy(self.bcache, self.blen[t], si.bq, self.bout, self.bscale, sets,
+                                        k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,
+                                        scores=self.scores, stream=stream)
+        else:
+            with _timer(timers, "base_attn", stream, only):
+                kvr.decode_attn(self.bcache, self.blen[t], si.bq, self.bout, self.bscale,
+                                k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,
+                                scores=self.scores, stream=stream)
+
     def helper_token(self, step: int, si: StepInputs, stream=None, timers=None, only=None) -> None:
         h = self.wl.helper
         with _timer(timers, "helper_attn", stream, only):
@@ -190,13 +206,17 @@ class Decoder:
                             k_new=si.hk, v_new=si.hv, prefix=self.prefix, workspace=self.hws,
                             stream=stream)
 
+    def logit_sets(self, si: StepInputs) -> list:
+        """The step's logit sets (the base set first, with the detector)."""
+        return [kvr.LogitSet(lg, self.H[w], self.wl.logits[w].V,
+                             detector=self.detector if w == 0 else None)
+                for w, lg in enumerate(si.logits)]
+
     def entropy(self, si: StepInputs, stream=None, timers=None, only=None) -> None:
         """Entropies of every logit set of the step in one batched call."""
         if not si.logits:
             return
-        sets = [kvr.LogitSet(lg, self.H[w], self.wl.logits[w].V,
-                             detector=self.detector if w == 0 else None)
-                for w, lg in enumerate(si.logits)]
+        sets = self.logit_sets(si)
         with _timer(timers, "entropy", stream, only):
             kvr.logit_entropy_batch(sets, workspace=self.ews_batch, stream=stream)
 
@@ -211,11 +231,14 @@ class Decoder:
         under its name; `evict_log` as for base_token."""
         t = self.T_prompt + step
         si = self.inputs(t)
+        fused = self.fuse_entropy and bool(si.logits)
         if self.wl.base:
-            self.base_token(t, si, stream, timers=timers, evict_log=evict_log, only=only)
+            self.base_token(t, si, stream, timers=timers, evict_log=evict_log, only=only,
+                            sets=self.logit_sets(si) if fused else None)
         if self.wl.helper:
             self.helper_token(step, si, stream, timers=timers, only=only)
-        self.entropy(si, stream, timers=timers, only=only)
+        if not fused:
+            self.entropy(si, stream, timers=timers, only=only)
 
 
 class _timer:

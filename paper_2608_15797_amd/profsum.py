@@ -40,9 +40,10 @@ CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 # Sources whose kernels each call runs (a record stays valid while they do not change).
 CALL_SOURCES = {
     "base_attn": ("attn.hip", "kvr_device.h"),
+    "base_attn_entropy": ("attn.hip", "entropy_common.h", "kvr_device.h"),
     "helper_attn": ("attn.hip", "kvr_device.h"),
     "evict": ("evict.hip", "kvr_device.h"),
-    "entropy": ("entropy.hip", "kvr_device.h"),
+    "entropy": ("entropy.hip", "entropy_common.h", "kvr_device.h"),
 }
 
 # Kernels launched by one call of each hot-path entry point, by call name; a
@@ -50,6 +51,7 @@ CALL_SOURCES = {
 # shapes (the entropy merge, absent when whole rows go to one workgroup).
 CALL_KERNELS = {
     "base_attn": (r"attn_cache_bf16<\d+, false",),
+    "base_attn_entropy": (r"attn_cache_bf16<\d+, false",),
     "helper_attn": (r"attn_prefix_bf16<", r"attn_cache_bf16<\d+, true"),
     "evict": (r"evict_topb_kernel",),
     "entropy": (r"entropy_kernel<", r"?entropy_merge"),

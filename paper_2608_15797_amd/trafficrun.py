@@ -40,8 +40,7 @@ def calibration_copy(nbytes: int = 1 << 30) -> None:
 def main(argv=None) -> None:
     import json
 
-    from paper_2608_15797_amd import accounting as acc
-    from paper_2608_15797_amd.benchplan import Schedule, cycle_steps, place_window, window_stats
+    from paper_2608_15797_amd.benchplan import Schedule, cycle_steps, place_window, step_bytes, window_stats
     from paper_2608_15797_amd.pipeline import Decoder
     from paper_2608_15797_amd.workloads import WORKLOADS
 
@@ -66,23 +65,13 @@ def main(argv=None) -> None:
         a[1] += 1
 
     def step(i, counted):
-        t = dec.T_prompt + i
-        si = dec.inputs(t)
-        if wl.base:
-            moved = []
-            if dec.base_token(t, si, evict_log=moved) and counted:
-                b = wl.base
-                count("evict", acc.evict_bytes(wl, dec.blen_host[t], moved[0] / (b.S * b.L * b.Hkv)))
-            if counted:
-                count("base_attn", acc.base_attn_bytes(wl, dec.blen_host[t]))
-        if wl.helper:
-            dec.helper_token(i, si)
-            if counted:
-                count("helper_attn", acc.helper_attn_bytes(wl, dec.hlen_host[i]))
-        if wl.logits:
-            dec.entropy(si)
-            if counted:
-                count("entropy", acc.entropy_bytes(wl))
+        moved = []
+        dec.step(i, evict_log=moved)
+        if counted:
+            b = wl.base
+            mr = moved[0] / (b.S * b.L * b.Hkv) if moved else None
+            for call, nbytes in step_bytes(wl, dec, i, mr).items():
+                count(call, nbytes)
 
     dec.prompt()
     for i in range(s0 - args.warmup, s0):

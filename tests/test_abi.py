@@ -211,3 +211,21 @@ def test_entropy_noalloc_rejects_on_host():
     assert f(None, 1, None) == -1
     arr[0] = kvr.c_logit_set(16, 1, 4, 10, 5, 1.0, 16, None)
     assert f(arr, 1, None) == -1
+
+
+def test_decode_attn_entropy_rejects_on_host():
+    """The fused attention + entropy call checks the attention arguments and
+    every logit set, and refuses rows that do not start 16-byte aligned."""
+    from paper_2608_15797_amd import kvr
+    f = kvr.lib.kvr_decode_attn_entropy
+    c = _cache(kvr)
+    arr = (kvr.c_logit_set * 1)()
+    arr[0] = kvr.c_logit_set(16, 1, 4, 1001, 1001, 1.0, 16, None)  # ld * 2 = 2002 bytes
+    assert f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1, None) == -1
+    assert "aligned" in kvr.lib.kvr_last_error().decode()
+    arr[0] = kvr.c_logit_set(16, 1, 4, 10, 5, 1.0, 16, None)  # ld < V
+    assert f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1, None) == -1
+    bad = _cache(kvr, D=96)
+    arr[0] = kvr.c_logit_set(16, 1, 4, 1024, 1024, 1.0, 16, None)
+    assert f(ctypes.byref(bad), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1, None) == -2
+    assert f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 1, None) == -1

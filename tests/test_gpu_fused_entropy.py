@@ -1,0 +1,136 @@
+"""kvr_decode_attn_entropy: base attention and the step's entropies in one
+launch, through the C ABI.
+
+The same inputs go through the fused call and through the two separate calls
+(kvr_decode_attn, then kvr_logit_entropy_batch): attention outputs, streamed
+scores and the appended cache rows must be bit for bit those of
+kvr_decode_attn (the attention lanes of the fused launch run the same code);
+every entropy must be within 1e-4 of the oracle, and the detector state
+(history, counts, flags) must follow the oracle's detector over three calls.
+Cases cover both cache types, bf16 and float32 logits, several sets with
+their own vocabulary, stride and temperature, a vocabulary below one 8-logit
+vector and one that is not a multiple of 8, -inf entries and a boosted row.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import as_f64, host, say
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+CASES = [
+    # cache (S, L, Hkv, G, D, B, W, buffer, dtype), logit dtype, sets [(R, V, ld, std, inv_temp, detector)]
+    ((4, 2, 4, 7, 128, 64, 32, 64, torch.bfloat16), torch.bfloat16,
+     [(16, 152064, 152064, 3.0, 1.0, True), (9, 151936, 152000, 1.0, 0.7, False)]),
+    ((3, 2, 2, 8, 128, 16, 4, 8, torch.bfloat16), torch.float32,
+     [(5, 1023, 1024, 2.0, 1.0, True), (3, 5, 8, 1.0, 1.0, False), (2, 8, 8, 0.5, 2.0, True)]),
+    ((2, 1, 2, 4, 64, 12, 4, 6, torch.bfloat16), torch.bfloat16, [(7, 50000, 50000, 2.0, 1.0, True)]),
+    ((1, 1, 1, 4, 64, 16, 8, 16, torch.float32), torch.float32, [(1, 1024, 1024, 2.0, 1.0, True)]),
+]
+
+
+def _randn(shape, g, dtype, std=1.0):
+    return (torch.randn(shape, generator=g, dtype=torch.float32) * std).to(dtype)
+
+
+@pytest.mark.parametrize("ci", range(len(CASES)))
+def test_decode_attn_entropy_matches_separate_calls(ci):
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_15797_amd import kvr as k
+    (S, L, Hkv, G, D, B, W, buffer, dt), ldt, specs = CASES[ci]
+    say("case", ci, "cache", CASES[ci][0], "logits", ldt, "sets", specs)
+    Hq = Hkv * G
+    cap = B + buffer + 1
+    wstart = B + buffer + 2 - W
+    g = torch.Generator().manual_seed(4242 + ci)
+    scale = 1.0 / math.sqrt(D)
+    K = _randn((S, L, Hkv, cap, D), g, dt)
+    V = _randn((S, L, Hkv, cap, D), g, dt)
+    pos = torch.randint(0, 999, (S, L, Hkv, cap), generator=g, dtype=torch.int32)
+    sc0 = torch.rand((S, L, Hkv, cap), generator=g) * 3
+    pol = k.Policy(B, W, buffer)
+
+    def caches():
+        return [k.Cache(K.to(DEV), V.to(DEV), pos.to(DEV)) for _ in range(2)]
+
+    ca, cb = caches()
+    sa, sb = sc0.to(DEV), sc0.to(DEV)
+    # Logit rows (with padding past V that must be ignored) and detectors.
+    xs = []
+    for R, V_, ld, std, it, det in specs:
+        x = torch.full((R, ld), 1e3)
+        x[:, :V_] = torch.randn((R, V_), generator=g) * std
+        if V_ > 20:
+            x[0, 3:9] = float("-inf")
+            x[-1, :5] += 10.0
+        xs.append(x.to(ldt))
+
+    def sets(tag):
+        return [k.LogitSet(x.to(DEV), torch.full((x.shape[0],), float("nan"), device=DEV), V_, it,
+                           k.Detector.zeros(x.shape[0], window=12, guard=1, tau=5.0, device=DEV) if det else None)
+                for x, (R, V_, ld, std, it, det) in zip(xs, specs)]
+
+    seta, setb = sets("a"), sets("b")
+    odets = [oracle.Detector(R, window=12, guard=1, tau=5.0) if det else None for R, V_, ld, std, it, det in specs]
+    need = k.logit_entropy_batch_workspace_size([(R, V_) for R, V_, *_ in specs], ldt)
+    ws = torch.zeros(max(need, 16) // 4, device=DEV)
+    Href = [oracle.entropy(host(x), V=V_, inv_temp=it) for x, (R, V_, ld, std, it, det) in zip(xs, specs)]
+    for step in range(3):
+        # Lengths: before, at and inside the observation window.
+        lens = [max(1, wstart - 2 + step), wstart + step, min(cap, wstart + 3 + step)][:S]
+        while len(lens) < S:
+            lens.append(min(cap, 1 + 7 * len(lens) + step))
+        lent = torch.tensor(lens, dtype=torch.int32, device=DEV)
+        q = _randn((S, L, Hq, D), g, dt).to(DEV)
+        kn = _randn((S, L, Hkv, D), g, dt).to(DEV)
+        vn = _randn((S, L, Hkv, D), g, dt).to(DEV)
+        npos = (torch.arange(S, dtype=torch.int32) + 1000 + step).to(DEV)
+        oa = torch.empty((S, L, Hq, D), dtype=dt, device=DEV)
+        ob = torch.empty_like(oa)
+        k.decode_attn(ca, lent, q, oa, scale, k_new=kn, v_new=vn, new_pos=npos, policy=pol, scores=sa)
+        k.logit_entropy_batch(seta, workspace=ws)
+        k.decode_attn_entropy(cb, lent, q, ob, scale, setb, k_new=kn, v_new=vn, new_pos=npos, policy=pol,
+                              scores=sb)
+        torch.cuda.synchronize()
+        assert torch.equal(oa.cpu().view(torch.int16) if dt == torch.bfloat16 else oa.cpu(),
+                           ob.cpu().view(torch.int16) if dt == torch.bfloat16 else ob.cpu())
+        assert torch.equal(sa.cpu(), sb.cpu())
+        for t in ("k", "v"):
+            x, y = getattr(ca, t).cpu(), getattr(cb, t).cpu()
+            assert torch.equal(x.view(torch.int16) if dt == torch.bfloat16 else x,
+                               y.view(torch.int16) if dt == torch.bfloat16 else y)
+        assert torch.equal(ca.pos.cpu(), cb.pos.cpu())
+        for j, (a, b, ref, od) in enumerate(zip(seta, setb, Href, odets)):
+            hb = b.H.cpu().double().numpy()
+            d = np.abs(hb - ref).max()
+            say("  step", step, "set", j, "max |fused - oracle|", d, "max |fused - batch|",
+                np.abs(hb - a.H.cpu().double().numpy()).max())
+            assert d <= 1e-4
+            if od is not None:
+                fref = od.step(ref)
+                assert b.detector.cnt.cpu().numpy().tolist() == [step + 1] * len(ref)
+                assert np.abs(b.detector.hist.cpu().double().numpy()[:, step] - ref).max() <= 1e-4
+                # Flags may differ only where the moving mean lies within 1e-4 of tau.
+                mean = od.hist[:, : step + 1].mean(axis=1)
+                f = b.detector.flag.cpu().numpy()
+                ok = (f == fref) | (np.abs(mean - 5.0) < 1e-4)
+                assert ok.all()
+
+
+def test_decode_attn_entropy_rejects_unaligned_rows():
+    from paper_2608_15797_amd import kvr as k
+    S, L, Hkv, G, D, cap = 2, 1, 1, 4, 128, 33
+    cache = k.Cache.empty(S, L, Hkv, cap, D, torch.bfloat16, DEV)
+    q = torch.zeros((S, L, Hkv * G, D), dtype=torch.bfloat16, device=DEV)
+    out = torch.empty_like(q)
+    lent = torch.ones(S, dtype=torch.int32, device=DEV)
+    x = torch.zeros((4, 1001), dtype=torch.bfloat16, device=DEV)  # ld * 2 = 2002 bytes
+    with pytest.raises(k.KvrError) as e:
+        k.decode_attn_entropy(cache, lent, q, out, 1.0, [k.LogitSet(x, torch.empty(4, device=DEV))])
+    assert e.value.status == -1 and "aligned" in str(e.value)
