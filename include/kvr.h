@@ -189,6 +189,11 @@ size_t kvr_decode_attn_workspace_size(const kvr_cache *cache, const kvr_prefix *
  *             rows r and the G query heads of KV head h of the probability of
  *             slot j (0 where row r cannot see j). accumulate != 0 adds to the
  *             stored value instead of overwriting. Slots >= len[s] untouched.
+ * Results are bitwise reproducible (the bf16 kernels sum the per-row-block
+ * contributions in 64-bit fixed point, 2^-32 resolution). Errors: as
+ * kvr_decode_attn, and KVR_EUNSUPPORTED when cap exceeds 8192 slots (bf16:
+ * one 8-byte accumulator per slot in 64 KiB of LDS) or (D + 2 cap) floats
+ * exceed 64 KiB (float32).
  */
 int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void *q_win,
                           int32_t nq, int32_t Hq, float scale, float *scores,

@@ -178,7 +178,7 @@ int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void
   if (Hq <= 0 || nq <= 0) return fail(KVR_EINVAL, "Hq and nq must be positive");
   if (!len || !q_win || !scores) return fail(KVR_EINVAL, "len, q_win and scores are required");
   const size_t lds = cache->dtype == KVR_BF16
-                        ? (size_t)cache->cap * sizeof(float)
+                        ? (size_t)cache->cap * sizeof(unsigned long long)
                         : ((size_t)cache->D + 2 * (size_t)cache->cap) * sizeof(float);
   if (lds > 65536) return fail(KVR_EUNSUPPORTED, "cap=%d needs too much LDS", cache->cap);
   if (!aligned16(q_win)) return fail(KVR_EINVAL, "q_win not 16-byte aligned");

@@ -13,9 +13,12 @@
 // the window rows and make two passes over the keys: the first builds every
 // row's softmax maximum and normaliser (online, per lane, then merged across
 // the 16 lanes holding the same rows), the second recomputes the logits, forms
-// the probabilities and adds their column sums into an LDS accumulator (LDS
-// float atomics, so the last bits may vary with the order of the waves). The
-// head's scores are written (or added) once at the end. The keys stream through
+// the probabilities and adds their column sums into an LDS accumulator. The
+// accumulator is 64-bit fixed point (each column sum rounded to a multiple of
+// 2^-32, then added with integer atomics), so the total does not depend on
+// the order in which the waves add: the scores are bitwise reproducible. The
+// head's scores are written (or added) once at the end, converted back to
+// float32. The keys stream through
 // an LDS ring shared by the workgroup's eight waves (window_scores_tiled);
 // caches too long for the ring beside the accumulator take the older kernel,
 // in which each wave of four streams K for its own two row blocks.
@@ -101,6 +104,17 @@ __device__ __forceinline__ short4_t s4(uint32_t a, uint32_t b) {
 
 constexpr float kNegInf = -__builtin_huge_valf();
 
+// Fixed-point column sums of the bf16 kernels: value * 2^32 as int64. A
+// column sum is at most G * nq (every window row's whole probability mass),
+// far below 2^31, and each addend is rounded once (to 2^-33 at worst).
+constexpr double kFix = 4294967296.0;
+__device__ __forceinline__ void fix_add(unsigned long long *acc, float v) {
+  atomicAdd(acc, (unsigned long long)__double2ll_rn((double)v * kFix));
+}
+__device__ __forceinline__ float fix_value(unsigned long long a) {
+  return (float)((double)(long long)a * (1.0 / kFix));
+}
+
 template <int D>
 struct WGeo {
   static constexpr int QD = D / 4;   // elements per lane quarter of a row
@@ -153,7 +167,7 @@ __device__ __forceinline__ void logits_tile_n(const short4_t (&qa)[NRB][WGeo<D>:
 
 template <int D>
 __global__ __launch_bounds__(256) void window_scores_bf16(ScoreParams p) {
-  extern __shared__ float acc[];  // [cap]
+  extern __shared__ unsigned long long acc[];  // [cap] fixed-point column sums
   const int unit = blockIdx.x;
   const int h = unit % p.Hkv;
   const int sl = unit / p.Hkv;
@@ -165,7 +179,7 @@ __global__ __launch_bounds__(256) void window_scores_bf16(ScoreParams p) {
   const int gq = lane >> 4, col = lane & 15;
   int n = p.len[s];
   n = n < 0 ? 0 : (n > p.cap ? p.cap : n);
-  for (int j = tid; j < n; j += blockDim.x) acc[j] = 0.f;
+  for (int j = tid; j < n; j += blockDim.x) acc[j] = 0ull;
   __syncthreads();
 
   const int R = p.G * p.nq;
@@ -263,12 +277,12 @@ __global__ __launch_bounds__(256) void window_scores_bf16(ScoreParams p) {
           if (j < nr[b][i] && iz[b][i] > 0.f) cs += fast_exp2(cc[b][i] * c - m[b][i]) * iz[b][i];
       cs += shfl_xor(cs, 16);
       cs += shfl_xor(cs, 32);
-      if (gq == 0 && j < n) atomicAdd(&acc[j], cs);
+      if (gq == 0 && j < n) fix_add(&acc[j], cs);
     }
   }
   __syncthreads();
   float *sc = p.scores + (size_t)unit * p.cap;
-  for (int j = tid; j < n; j += blockDim.x) sc[j] = p.accumulate ? sc[j] + acc[j] : acc[j];
+  for (int j = tid; j < n; j += blockDim.x) sc[j] = p.accumulate ? sc[j] + fix_value(acc[j]) : fix_value(acc[j]);
 }
 
 // LDS-tiled variant. A workgroup of NW waves holds NW * KRB 16-row blocks of
@@ -301,7 +315,7 @@ __global__ __launch_bounds__(NW * 64) void window_scores_tiled(ScoreParams p) {
   constexpr int NI = TB / 1024;         // 1 KiB buffer-to-LDS loads per tile
   constexpr int RPI = 1024 / (D * 2);   // key rows per load
   extern __shared__ float smem[];
-  float *acc = smem;                    // [cap] column sums
+  unsigned long long *acc = reinterpret_cast<unsigned long long *>(smem);  // [cap] fixed-point column sums
   const int unit = blockIdx.x;
   const int h = unit % p.Hkv;
   const int sl = unit / p.Hkv;
@@ -313,8 +327,8 @@ __global__ __launch_bounds__(NW * 64) void window_scores_tiled(ScoreParams p) {
   const int gq = lane >> 4, col = lane & 15;
   int n = p.len[s];
   n = n < 0 ? 0 : (n > p.cap ? p.cap : n);
-  char *ring = reinterpret_cast<char *>(smem + ((p.cap + 3) & ~3));  // [2][TB], 16-byte aligned
-  for (int j = tid; j < n; j += NW * kWave) acc[j] = 0.f;
+  char *ring = reinterpret_cast<char *>(acc + ((p.cap + 1) & ~1));  // [2][TB], 16-byte aligned
+  for (int j = tid; j < n; j += NW * kWave) acc[j] = 0ull;
   __syncthreads();
 
   const int R = p.G * p.nq;
@@ -465,18 +479,18 @@ __global__ __launch_bounds__(NW * 64) void window_scores_tiled(ScoreParams p) {
           if (j < nr[b][i] && z[b][i] > 0.f) cs += fast_exp2(cc[b][i] * c - m[b][i]) * z[b][i];
       cs += shfl_xor(cs, 16);
       cs += shfl_xor(cs, 32);
-      if (gq == 0 && j < n) atomicAdd(&acc[j], cs);
+      if (gq == 0 && j < n) fix_add(&acc[j], cs);
     });
   }
   __syncthreads();
   float *sc = p.scores + (size_t)unit * p.cap;
-  for (int j = tid; j < n; j += NW * kWave) sc[j] = p.accumulate ? sc[j] + acc[j] : acc[j];
+  for (int j = tid; j < n; j += NW * kWave) sc[j] = p.accumulate ? sc[j] + fix_value(acc[j]) : fix_value(acc[j]);
 }
 
 }  // namespace
 
 size_t window_scores_tiled_lds_bytes(int cap, int D) {
-  return ((size_t)((cap + 3) & ~3)) * sizeof(float) + 2 * (size_t)kTK * D * 2;
+  return ((size_t)((cap + 1) & ~1)) * sizeof(unsigned long long) + 2 * (size_t)kTK * D * 2;
 }
 
 hipError_t launch_accumulate_scores(const ScoreParams &p, hipStream_t stream) {
@@ -492,7 +506,7 @@ hipError_t launch_accumulate_scores(const ScoreParams &p, hipStream_t stream) {
     } else {
       // Caches too long for the ring beside the accumulator: one wave streams
       // K per two row blocks (more K traffic, same result).
-      const size_t lds = (size_t)p.cap * sizeof(float);
+      const size_t lds = (size_t)p.cap * sizeof(unsigned long long);
       if (p.D == 128) hipLaunchKernelGGL(window_scores_bf16<128>, grid, dim3(256), lds, stream, p);
       else hipLaunchKernelGGL(window_scores_bf16<64>, grid, dim3(256), lds, stream, p);
     }

@@ -193,9 +193,11 @@ def test_lds_limits_rejected_on_host():
     c = _cache(kvr, cap=8100)
     pol = kvr.c_policy(256, 32, 7843)
     assert kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, 16, ctypes.byref(pol), None, None) == -2
-    # Window recompute (bf16): cap words of LDS.
-    c = _cache(kvr, cap=16385)
+    # Window recompute (bf16): one 64-bit fixed-point accumulator per slot.
+    c = _cache(kvr, cap=8193)
     assert kvr.lib.kvr_accumulate_scores(ctypes.byref(c), 16, 16, 8, 8, 1.0, 16, 0, None) == -2
+    c = _cache(kvr, cap=8192, k=0, v=0)  # within the limit: fails later, on the NULL cache pointers
+    assert kvr.lib.kvr_accumulate_scores(ctypes.byref(c), 16, 16, 8, 8, 1.0, 16, 0, None) == -1
 
 
 def test_entropy_noalloc_rejects_on_host():

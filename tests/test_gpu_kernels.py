@@ -346,9 +346,9 @@ def test_evict_topb_ties_and_gpu_scores_selection():
     (torch.bfloat16, 128, 16, 33, 130),    # 33 row blocks: the last pair is half empty
     (torch.bfloat16, 128, 1, 3, 40),       # fewer rows than one block
     (torch.bfloat16, 128, 7, 128, 300),    # a committed step's window on the 7B head shape
-    (torch.bfloat16, 128, 4, 8, 12288),    # largest cache of the LDS-ring kernel: accumulator + ring = 64 KB
-    (torch.bfloat16, 64, 4, 8, 15000),     # beyond it at D = 64: the single-wave-stream kernel
-    (torch.bfloat16, 128, 4, 8, 16384),    # largest cache: the accumulator alone fills 64 KB of LDS
+    (torch.bfloat16, 128, 4, 8, 6144),     # largest cache of the LDS-ring kernel: 64-bit accumulator + ring = 64 KB
+    (torch.bfloat16, 64, 4, 8, 7500),      # beyond it at D = 64: the single-wave-stream kernel
+    (torch.bfloat16, 128, 4, 8, 8192),     # largest cache: the accumulator alone fills 64 KB of LDS
 ])
 def test_accumulate_scores(dt, D, G, nq, cap):
     """kvr_accumulate_scores equals the oracle's causal window re-computation,
@@ -372,11 +372,19 @@ def test_accumulate_scores(dt, D, G, nq, cap):
     for s, n in enumerate(lens):
         assert np.abs(got[s, ..., :n] - ref[s, ..., :n]).max() <= 1e-4
         assert (got[s, ..., n:] == 0.25).all()
+    first = sc.clone()
     k.accumulate_scores(cache, lent, qw.to(DEV), scale, sc, accumulate=True)
     torch.cuda.synchronize()
     got = sc.cpu().double().numpy()
     for s, n in enumerate(lens):
         assert np.abs(got[s, ..., :n] - 2 * ref[s, ..., :n]).max() <= 2e-4
+    # Bitwise reproducible: the same call again gives the same bits (the
+    # column sums of the workgroup's waves are added in fixed point).
+    for _ in range(3):
+        again = torch.full((S, L, Hkv, cap), 0.25, device=DEV)
+        k.accumulate_scores(cache, lent, qw.to(DEV), scale, again, accumulate=False)
+        torch.cuda.synchronize()
+        assert torch.equal(again.view(torch.int32), first.view(torch.int32))
 
 
 # ------------------------------------------------------------ entropy
