@@ -1084,17 +1084,19 @@ hipError_t launch_bf16(const AttnParams &p_in, const EntropyBatch *ent, hipStrea
   }
   const dim3 units(p.S * p.L * p.Hkv);
   if (p.P == 0) {
-    // At D = 128 the kernel asks for at least 26 KiB of LDS, which caps it at
-    // 6 single-wave workgroups per CU (160 KiB) instead of the 8 its registers
-    // allow: fewer concurrent short K/V streams measured 2.5-3.5% faster
-    // (5 per CU lost at short caches, 7 matched 6).
+    // Register-resident keys (the fallback when the LDS ring and the window
+    // logits do not fit): at D = 128 the kernel asks for at least 26 KiB of
+    // LDS, which caps it at 6 single-wave workgroups per CU (160 KiB) instead
+    // of the 8 its registers allow: fewer concurrent short K/V streams
+    // measured 2.5-3.5% faster (5 per CU lost at short caches, 7 matched 6).
     const size_t logits = p.scores ? ((size_t)p.G * ((p.cap + 63) & ~63) + 32) * sizeof(float) : 0;
     const size_t lds_min = D == 128 ? kBaseLdsFloor : 0;
     constexpr size_t ring = kl_ring<D, kKlTiles, kKlDepth>;
     if (ring + logits <= kMaxLds) {
-      // Key rows through the LDS ring.
-      const size_t need = ring + logits;
-      launch_own<D, kKlTiles, kKlDepth, true>(p, ent, need > lds_min ? need : lds_min, stream);
+      // Key rows through the LDS ring. No floor here: with the keys in LDS,
+      // 7-8 workgroups per CU (registers: 172) measured 1-1.5% faster than the
+      // 6 of a 26 KiB floor on the 7B shapes and equal on the 72B shape.
+      launch_own<D, kKlTiles, kKlDepth, true>(p, ent, ring + logits, stream);
     } else {
       launch_own<D, 2, 2, false>(p, ent, logits > lds_min ? logits : lds_min, stream);
     }
