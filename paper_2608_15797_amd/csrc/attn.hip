@@ -378,7 +378,6 @@ __device__ __forceinline__ short4_t make_vop(const uint32_t (&v)[4][Geo<D>::VW],
   return s4(__builtin_amdgcn_perm(v[1][w], v[0][w], sel), __builtin_amdgcn_perm(v[3][w], v[2][w], sel));
 }
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // Four probabilities -> A operand of P.V (hardware round-to-nearest-even).
