@@ -692,10 +692,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
       const float mi = __shfl(st.m, row, kWave);
       if (i == 0) wait_vm0();  // the LDS copies of the partials have landed
       if (row < G) {
-        // Piece k of this row's record: in LDS for k < pf, else in the workspace.
-        auto rec = [&](int k) -> const float * {
-          return k < pf ? smem + k * p.merge_blk + row * RF : rbase + k * rstride + row * RF;
-        };
         if (npieces <= kFastPieces && npieces <= pf) {
           // Every piece is in LDS: all of its reads are issued before any is
           // used, so the row's merge costs one LDS round trip.
@@ -740,14 +736,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
             }
           }
         } else {
+        // Pieces k < pf from LDS, the others from the workspace, in loops of
+        // their own so that each reads through its own memory path (one loop
+        // over a pointer into either would read through flat addressing and
+        // wait for every access in turn).
         float M = mi;
-        for (int k = 0; k < npieces; k++) M = fmaxf(M, rec(k)[0]);
+        for (int k = 0; k < pf; k++) M = fmaxf(M, smem[k * p.merge_blk + row * RF]);
+        for (int k = pf; k < npieces; k++) M = fmaxf(M, rbase[k * rstride + row * RF]);
         const float wown = fast_exp2(mi - M);
         zi *= wown;
 #pragma unroll
         for (int b = 0; b < NB; b++) o[b][i] *= wown;
-        for (int k = 0; k < npieces; k++) {
-          const float *r = rec(k);
+        auto fold = [&](const float *r) {
           const float mk = r[0];
           const float w = mk == kNegInf ? 0.0f : r[1] * fast_exp2(mk - M);
           zi += w;
@@ -765,7 +765,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
             o[2 * b][i] += f16_lo(hv[b]) * w;
             o[2 * b + 1][i] += f16_hi(hv[b]) * w;
           }
-        }
+        };
+        for (int k = 0; k < pf; k++) fold(smem + k * p.merge_blk + row * RF);
+        for (int k = pf; k < npieces; k++) fold(rbase + k * rstride + row * RF);
         }
       }
     }
