@@ -537,6 +537,7 @@ def main():
         "ms_per_step": res["ms_per_step"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded, Qwen2.5-Math shapes)",
         "config": cfg, "roofline": roof, "cpu_baseline": cpu,
+        "entropy_marginal": res.get("entropy_marginal"),
         "cycle": res.get("cycle"), "workloads": extra, "sampler": sampler,
         "copy_ref_GBps": copy_ref,
     }

@@ -50,8 +50,10 @@ CALL_SOURCES = {
 # pattern starting with "?" names a kernel the call launches only for some
 # shapes (the entropy merge, absent when whole rows go to one workgroup).
 CALL_KERNELS = {
-    "base_attn": (r"attn_cache_bf16<\d+, false",),
-    "base_attn_entropy": (r"attn_cache_bf16<\d+, false",),
+    # The evicted-cache kernel without entropy rows (last template argument 0)
+    # and with them (1: bf16 logits, 2: float32 logits).
+    "base_attn": (r"attn_cache_bf16<\d+, false, \d+, \d+, (true|false), 0>",),
+    "base_attn_entropy": (r"attn_cache_bf16<\d+, false, \d+, \d+, (true|false), [12]>",),
     "helper_attn": (r"attn_prefix_bf16<", r"attn_cache_bf16<\d+, true"),
     "evict": (r"evict_topb_kernel",),
     "entropy": (r"entropy_kernel<", r"?entropy_merge"),
