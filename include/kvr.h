@@ -205,16 +205,22 @@ int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void
  *
  * For every sequence with n = len[s] > B + buffer, and every (layer, KV head)
  * independently: the W newest slots [n-W, n) are kept; of the slots [0, n-W)
- * the B-W with the largest scores are kept, ties going to the lower slot. The
- * kept rows of k, v (and pos) move to slots 0..B-1 in their original order.
- * Sequences with len[s] <= B + buffer are not touched. The caller sets the new
- * live length B for evicted sequences.
+ * the B-W with the largest scores are kept, ties going to the lower slot
+ * (selected by a wavefront radix select on the scores' order-preserving
+ * 32-bit keys). The kept rows of k, v (and pos) move to slots 0..B-1 in their
+ * original order. Sequences with len[s] <= B + buffer are not touched.
  *
- *   scores : [S][L][Hkv][cap] float32 importance scores (read only).
- *   kept   : NULL or [S][L][Hkv][B] int32, receives the kept pre-eviction slot
- *            ids in ascending order for evicted sequences.
+ *   len     : [S] int32 device, live lengths (read only).
+ *   len_out : NULL, or [S] int32 device receiving the new live lengths: B for
+ *             evicted sequences, len[s] for the others. Must not overlap len
+ *             (KVR_EINVAL). Callers that track lengths themselves pass NULL.
+ *   scores  : [S][L][Hkv][cap] float32 importance scores (read only).
+ *   kept    : NULL or [S][L][Hkv][B] int32, receives the kept pre-eviction
+ *             slot ids in ascending order for evicted sequences.
+ * Errors: KVR_EINVAL (shape, pointer, policy, overlap), KVR_EUNSUPPORTED (D,
+ * dtype, cap + B above 16384 slots of LDS), KVR_EHIP.
  */
-int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scores,
+int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, int32_t *len_out, const float *scores,
                    const kvr_policy *policy, int32_t *kept, hipStream_t stream);
 
 /*

@@ -193,20 +193,25 @@ int kvr_accumulate_scores(const kvr_cache *cache, const int32_t *len, const void
   return hip_status(kvr::launch_accumulate_scores(p, stream), "kvr_accumulate_scores launch");
 }
 
-int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, const float *scores,
+int kvr_evict_topb(const kvr_cache *cache, const int32_t *len, int32_t *len_out, const float *scores,
                    const kvr_policy *policy, int32_t *kept, hipStream_t stream) {
   int G = 0;
   int st = check_cache(cache, 0, &G);
   if (st) return st;
   if (!len || !scores || !policy) return fail(KVR_EINVAL, "len, scores and policy are required");
+  if (len_out) {
+    const char *a = reinterpret_cast<const char *>(len), *b = reinterpret_cast<const char *>(len_out);
+    const size_t n = (size_t)cache->S * sizeof(int32_t);
+    if (a < b + n && b < a + n) return fail(KVR_EINVAL, "len_out overlaps len");
+  }
   st = check_policy(policy, cache->cap);
   if (st) return st;
-  const size_t lds = (size_t)(2 * cache->cap + policy->B) * sizeof(uint32_t);
+  const size_t lds = (size_t)(cache->cap + policy->B) * sizeof(uint32_t);
   if (lds > 65536) return fail(KVR_EUNSUPPORTED, "cap=%d needs too much LDS", cache->cap);
   kvr::EvictParams p{};
   p.k = cache->k; p.v = cache->v; p.pos = cache->pos;
   p.S = cache->S; p.L = cache->L; p.Hkv = cache->Hkv; p.cap = cache->cap; p.D = cache->D;
-  p.dtype = cache->dtype; p.len = len; p.scores = scores;
+  p.dtype = cache->dtype; p.len = len; p.len_out = len_out; p.scores = scores;
   p.B = policy->B; p.W = policy->W; p.buffer = policy->buffer; p.kept = kept;
   return hip_status(kvr::launch_evict_topb(p, stream), "kvr_evict_topb launch");
 }

@@ -2,12 +2,19 @@
 // (Eq. (1), first two lines), one workgroup per (sequence, layer, KV head).
 //
 // Selection: of the candidate slots [0, n-W) keep the B-W with the largest
-// score, ties to the lower slot. Each candidate's rank under the strict total
-// order (score desc, slot asc) is counted directly against all others held in
-// LDS; rank < B-W means kept. Scores are compared through an order-preserving
-// map of their float32 bit patterns, so the ranks form a permutation and
-// exactly B-W slots are kept even for unusual inputs. The window [n-W, n) is
-// always kept.
+// score, ties to the lower slot. Scores are compared through an order-
+// preserving map of their float32 bit patterns (32-bit keys), so the order
+// (key desc, slot asc) is strict and exactly B-W slots are kept even for
+// unusual inputs. One wavefront finds the threshold key T, the (B-W)-th
+// largest, by a bitwise radix select from the most significant bit: at each
+// bit it counts (ballot + popcount) the candidates that match T's bits
+// decided so far and have this bit set; if they are at least the number still
+// wanted the bit of T is 1, else they are all kept and the count wanted drops
+// by theirs. That is 32 ballot rounds over n-W keys (held in registers up to
+// 256 candidates), O(n) work where counting every candidate's rank against
+// all others is O(n^2). The kept slots are then the keys above T and the
+// lowest-slot keys equal to T, and their destinations a ballot prefix count
+// in slot order. The window [n-W, n) is always kept.
 //
 // Compaction: kept slot k_i moves to slot i. Since k_i >= i, destinations are
 // processed in ascending chunks of one 16-byte item of K and one of V per
@@ -29,12 +36,16 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Order-preserving 32-bit key of a float32 score; -0 and +0 map to one key
+// (they compare equal, so their tie goes to the lower slot).
 __device__ __forceinline__ uint32_t order_key(float f) {
-  const uint32_t u = __float_as_uint(f);
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
 constexpr int kThreads = 256;
+constexpr int kRegKeys = 4;  // candidate keys per lane held in registers by the select (n - W <= 256)
 constexpr int kItems = 1;  // 16-byte items per thread per tensor per chunk
 
 __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int row_units) {
@@ -42,6 +53,8 @@ __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int
   const int unit = blockIdx.x;  // ((s * L) + l) * Hkv + h
   const int s = unit / (p.L * p.Hkv);
   int n = p.len[s];
+  if (p.len_out && unit % (p.L * p.Hkv) == 0 && threadIdx.x == 0)
+    p.len_out[s] = n > p.B + p.buffer ? p.B : n;
   if (n <= p.B + p.buffer) return;
   if (n > p.cap) n = p.cap;
   const int tid = threadIdx.x;
@@ -49,8 +62,7 @@ __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int
   const int take = p.B - p.W;
 
   uint32_t *key = lds;                                    // [cap]
-  int *flag = reinterpret_cast<int *>(lds + p.cap);       // [cap]
-  int *kept = reinterpret_cast<int *>(lds + 2 * p.cap);   // [B]
+  int *kept = reinterpret_cast<int *>(lds + p.cap);       // [B]
   __shared__ int first_moved;
 
   const float *sc = p.scores + (size_t)unit * p.cap;
@@ -58,21 +70,51 @@ __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int
   if (tid == 0) first_moved = p.B;
   __syncthreads();
 
-  for (int j = tid; j < nc; j += kThreads) {
-    const uint32_t kj = key[j];
-    int rank = 0;
-    for (int i = 0; i < nc; i++) {
-      const uint32_t ki = key[i];
-      rank += (ki > kj) | ((ki == kj) & (i < j));
+  if (tid < kWave) {
+    // Candidate j = 64 r + lane; keys past nc are never counted.
+    const int lane = tid;
+    const uint64_t below = (1ull << lane) - 1ull;
+    const bool inreg = nc <= kWave * kRegKeys;
+    uint32_t kr[kRegKeys];
+#pragma unroll
+    for (int r = 0; r < kRegKeys; r++) kr[r] = (inreg && kWave * r + lane < nc) ? key[kWave * r + lane] : 0u;
+    uint32_t T = 0u;
+    int need = take;  // >= 1: nc >= B > B - W
+    for (int bit = 31; bit >= 0; bit--) {
+      const uint32_t hi = ~((2u << bit) - 1u);  // the bits of T decided so far (none at bit 31)
+      const uint32_t want = T & hi;
+      int c = 0;
+      if (inreg) {
+#pragma unroll
+        for (int r = 0; r < kRegKeys; r++)
+          c += __popcll(__ballot(kWave * r + lane < nc && (kr[r] & hi) == want && ((kr[r] >> bit) & 1u)));
+      } else {
+        for (int j0 = 0; j0 < nc; j0 += kWave) {
+          const int j = j0 + lane;
+          const uint32_t k = j < nc ? key[j] : 0u;
+          c += __popcll(__ballot(j < nc && (k & hi) == want && ((k >> bit) & 1u)));
+        }
+      }
+      if (c >= need) T |= 1u << bit;
+      else need -= c;
     }
-    flag[j] = rank < take;
-  }
-  __syncthreads();
-  for (int j = tid; j < nc; j += kThreads) {
-    if (flag[j]) {
-      int dst = 0;
-      for (int i = 0; i < j; i++) dst += flag[i];
-      kept[dst] = j;
+    // Keep every key above T and the `need` lowest-slot keys equal to T, in
+    // slot order: destination = kept candidates before this one.
+    int base = 0, eq_seen = 0;
+    for (int j0 = 0; j0 < nc; j0 += kWave) {
+      const int j = j0 + lane;
+      const uint32_t k = j < nc ? (inreg ? kr[0] : key[j]) : 0u;
+      const bool eq = j < nc && k == T;
+      const uint64_t eqm = __ballot(eq);
+      const bool keep = j < nc && (k > T || (eq && eq_seen + __popcll(eqm & below) < need));
+      const uint64_t km = __ballot(keep);
+      if (keep) kept[base + __popcll(km & below)] = j;
+      base += __popcll(km);
+      eq_seen += __popcll(eqm);
+      if (inreg) {
+#pragma unroll
+        for (int r = 0; r + 1 < kRegKeys; r++) kr[r] = kr[r + 1];
+      }
     }
   }
   for (int w = tid; w < p.W; w += kThreads) kept[take + w] = nc + w;
@@ -132,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void evict_topb_kernel(EvictParams p, int
 hipError_t launch_evict_topb(const EvictParams &p, hipStream_t stream) {
   const int esz = p.dtype == 0 ? 4 : 2;
   const int row_units = p.D * esz / 16;
-  const size_t lds = (size_t)(2 * p.cap + p.B) * sizeof(uint32_t);
+  const size_t lds = (size_t)(p.cap + p.B) * sizeof(uint32_t);
   hipLaunchKernelGGL(evict_topb_kernel, dim3(p.S * p.L * p.Hkv), dim3(kThreads), lds, stream, p,
                      row_units);
   return hipGetLastError();

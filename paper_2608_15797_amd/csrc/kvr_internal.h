@@ -66,6 +66,7 @@ struct EvictParams {
   int32_t *pos;
   int S, L, Hkv, cap, D, dtype;
   const int32_t *len;
+  int32_t *len_out;  // NULL, or [S] new live lengths
   const float *scores;
   int B, W, buffer;
   int32_t *kept;

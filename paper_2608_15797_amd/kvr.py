@@ -86,7 +86,7 @@ def _load():
     lib.kvr_decode_attn_workspace_size.restype = sz
     lib.kvr_accumulate_scores.argtypes = [P(c_cache), vp, vp, i32, i32, f32, vp, i32, vp]
     lib.kvr_accumulate_scores.restype = ctypes.c_int
-    lib.kvr_evict_topb.argtypes = [P(c_cache), vp, vp, P(c_policy), vp, vp]
+    lib.kvr_evict_topb.argtypes = [P(c_cache), vp, vp, vp, P(c_policy), vp, vp]
     lib.kvr_evict_topb.restype = ctypes.c_int
     lib.kvr_logit_entropy.argtypes = [vp, i32, i32, i32, i64, f32, vp, P(c_detector), vp, sz, vp]
     lib.kvr_logit_entropy.restype = ctypes.c_int
@@ -270,11 +270,13 @@ def accumulate_scores(cache: Cache, len_: torch.Tensor, q_win: torch.Tensor, sca
 
 
 def evict_topb(cache: Cache, len_: torch.Tensor, scores: torch.Tensor, policy: Policy,
-               kept: Optional[torch.Tensor] = None, stream=None) -> None:
-    """kvr_evict_topb: in-place compaction of sequences with len > B + buffer."""
+               kept: Optional[torch.Tensor] = None, len_out: Optional[torch.Tensor] = None,
+               stream=None) -> None:
+    """kvr_evict_topb: in-place compaction of sequences with len > B + buffer;
+    len_out (optional) receives the new live lengths."""
     cc = cache.c()
     pol = policy.c()
-    rc = lib.kvr_evict_topb(ctypes.byref(cc), _ptr(len_), _ptr(scores), ctypes.byref(pol),
+    rc = lib.kvr_evict_topb(ctypes.byref(cc), _ptr(len_), _ptr(len_out), _ptr(scores), ctypes.byref(pol),
                             _ptr(kept), _stream(stream))
     _check(rc, "kvr_evict_topb")
 

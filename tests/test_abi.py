@@ -64,8 +64,14 @@ def test_policy_validation_on_host():
     c = _cache(kvr, cap=20)
     for pol, msg in ((kvr.c_policy(16, 8, 16), "cap="), (kvr.c_policy(16, 0, 4), "0 < W < B"),
                      (kvr.c_policy(8, 4, 2), "buffer >= W-1")):
-        rc = kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, 16, ctypes.byref(pol), None, None)
+        rc = kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, None, 16, ctypes.byref(pol), None, None)
         assert rc == -1 and msg in kvr.lib.kvr_last_error().decode()
+    # len_out must not overlap len ([S] int32 each; S = 2 here).
+    c = _cache(kvr, cap=40)
+    pol = kvr.c_policy(16, 8, 16)
+    for lo in (16, 12, 20):
+        rc = kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, lo, 16, ctypes.byref(pol), None, None)
+        assert rc == -1 and "overlaps" in kvr.lib.kvr_last_error().decode()
 
 
 def test_entropy_rejects_bad_arguments_on_host():
@@ -189,10 +195,10 @@ def test_lds_limits_rejected_on_host():
     rc = kvr.lib.kvr_decode_attn(ctypes.byref(c), None, 16, 16, 16, 1.0, None, None, None, 16,
                                  ctypes.byref(pol), 16, None, 0, None)
     assert rc == -2 and "LDS" in kvr.lib.kvr_last_error().decode()
-    # Eviction: (2 cap + B) words of LDS.
-    c = _cache(kvr, cap=8100)
-    pol = kvr.c_policy(256, 32, 7843)
-    assert kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, 16, ctypes.byref(pol), None, None) == -2
+    # Eviction: (cap + B) words of LDS, at most 16384.
+    c = _cache(kvr, cap=16129)
+    pol = kvr.c_policy(256, 32, 15872)
+    assert kvr.lib.kvr_evict_topb(ctypes.byref(c), 16, None, 16, ctypes.byref(pol), None, None) == -2
     # Window recompute (bf16): one 64-bit fixed-point accumulator per slot.
     c = _cache(kvr, cap=8193)
     assert kvr.lib.kvr_accumulate_scores(ctypes.byref(c), 16, 16, 8, 8, 1.0, 16, 0, None) == -2

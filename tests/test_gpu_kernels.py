@@ -263,9 +263,11 @@ def test_evict_topb_planted(case):
     sc = planted_scores((S, L, Hkv, cap), cap - W, g)
     cache = k.Cache(K.clone().to(DEV), V.clone().to(DEV), pos.clone().to(DEV))
     kept = torch.full((S, L, Hkv, B), -1, dtype=torch.int32, device=DEV)
+    len_out = torch.full((S,), -7, dtype=torch.int32, device=DEV)
     k.evict_topb(cache, torch.tensor(lens, dtype=torch.int32, device=DEV), sc.to(DEV),
-                 k.Policy(B, W, buffer), kept=kept)
+                 k.Policy(B, W, buffer), kept=kept, len_out=len_out)
     torch.cuda.synchronize()
+    assert len_out.cpu().tolist() == [B if n > B + buffer else n for n in lens]
     Kg, Vg, pg, kg = host(cache.k), host(cache.v), cache.pos.cpu().numpy(), kept.cpu().numpy()
     Kh, Vh, ph = host(K).copy(), host(V).copy(), pos.numpy().copy()
     scn = sc.double().numpy()
@@ -317,13 +319,17 @@ def test_evict_topb_planted_full_shape(S, L, Hkv, B, W, buffer):
     assert torch.equal(Kg, (torch.from_numpy(kg).float() * 0.5)[..., None].expand_as(Kg).to(torch.bfloat16).float())
 
 
-def test_evict_topb_ties_and_gpu_scores_selection():
-    """Exact ties go to the lower slot (integer-valued scores)."""
+@pytest.mark.parametrize("B,W,buffer,levels", [(24, 6, 10, 3), (128, 32, 300, 5), (64, 32, 64, 1)])
+def test_evict_topb_ties_and_gpu_scores_selection(B, W, buffer, levels):
+    """Exact ties go to the lower slot (integer-valued scores, signed and
+    with -0 next to +0); 97 candidates (select keys in registers) and 397
+    (keys re-read from LDS); one level: every score equal."""
     k = kvr()
-    S, L, Hkv, D, B, W, buffer = 2, 2, 2, 128, 24, 6, 10
+    S, L, Hkv, D = 2, 2, 2, 128
     cap = B + buffer + 1
-    g = torch.Generator().manual_seed(77)
-    sc = torch.randint(0, 3, (S, L, Hkv, cap), generator=g).float()
+    g = torch.Generator().manual_seed(77 + buffer)
+    sc = (torch.randint(0, levels, (S, L, Hkv, cap), generator=g) - levels // 2).float()
+    sc[0, 0, 0, ::7] = -0.0
     cache = k.Cache.empty(S, L, Hkv, cap, D, torch.bfloat16, DEV)
     kept = torch.empty((S, L, Hkv, B), dtype=torch.int32, device=DEV)
     k.evict_topb(cache, torch.full((S,), cap, dtype=torch.int32, device=DEV), sc.to(DEV),
