@@ -464,6 +464,8 @@ __device__ __forceinline__ void softmax_pv(float (&x)[TILES][4], RowState &st, f
 constexpr size_t kBaseLdsFloor = 26 * 1024;  // see the evicted-cache launch
 constexpr size_t kMaxLds = 64 * 1024;        // LDS a workgroup may ask for
 constexpr int kFastPieces = 4;  // split partials per row merged with batched LDS reads
+constexpr size_t kMergePrefetchBytes = 16384;  // LDS for the suffix kernel's prefetched partials
+constexpr bool kSuffixKl = true;               // suffix kernel with its key rows through the LDS ring
 
 // KL (evicted cache only): key rows through an LDS ring (load_chunk_lds)
 // instead of registers; the ring takes the first kl_ring<D, TILES, DEPTH>
@@ -483,7 +485,6 @@ constexpr int kKlDepth = 2;
 template <int D, bool MERGE, int TILES, int DEPTH, bool KL = false, int LT = 0>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void attn_cache_bf16(AttnParams p,
                                                                                                EntropyBatch e) {
-  static_assert(!(KL && MERGE), "LDS key rows are for the evicted cache");
   static_assert(!(LT && MERGE), "entropy rows ride with the evicted cache");
   constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
@@ -536,6 +537,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
   KVChunk<D, TILES> ring[KL ? 1 : DEPTH];
   VChunk<D, TILES> vring[KL ? DEPTH : 1];
   char *kring = reinterpret_cast<char *>(smem);  // KL: [DEPTH][CH rows of ROW bytes]
+  float *pbuf = smem + (KL ? kl_ring<D, TILES, DEPTH> / sizeof(float) : 0);  // MERGE: prefetched partials
   const KLOffsets<D, TILES> kloff(lane);
   if constexpr (!MERGE) {
     const int first = p.cap < CH ? p.cap : CH;
@@ -574,7 +576,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
     for (int k = 0; k < pf; k++) {
       const rsrc_t rr = make_rsrc(rbase + k * rstride, (uint32_t)G * RF * 4u);
       for (int j = 0; j < p.merge_blk / 256; j++)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void_t *)(smem + k * p.merge_blk + j * 256), 16,
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void_t *)(pbuf + k * p.merge_blk + j * 256), 16,
                                                  (uint32_t)(j * 1024 + lane * 16), 0, 0, 0);
     }
 #endif
@@ -665,7 +667,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
       softmax_pv<D, 1>(x, st, o, cn.v, g4);
     }
   };
-  if constexpr (MERGE) load_chunk<D, TILES>(ring[0], Kr, Vr, 0, r16, g4);
+  if constexpr (MERGE) {
+    if constexpr (KL)
+      load_chunk_lds<D, TILES>(vring[0], kring, Kc, Vc, ncache, 0, kloff);
+    else
+      load_chunk<D, TILES>(ring[0], Kr, Vr, 0, r16, g4);
+  }
   if constexpr (KL)
     stream_chunks_lds<D, TILES, DEPTH>(vring, kring, Kc, Vc, 0, ncache, kloff, new_token,
                                        [&](VChunk<D, TILES> &c, const char *slot, int c0) { process(c, slot, c0, ncache); });
@@ -700,7 +707,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
 #pragma unroll
           for (int k = 0; k < kFastPieces; k++) {
             if (k < npieces) {
-              const float *r = smem + k * p.merge_blk + row * RF;
+              const float *r = pbuf + k * p.merge_blk + row * RF;
               const float2_t ms = *reinterpret_cast<const float2_t *>(r);
               rm[k] = ms.x;
               rs[k] = ms.y;
@@ -741,7 +748,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
         // over a pointer into either would read through flat addressing and
         // wait for every access in turn).
         float M = mi;
-        for (int k = 0; k < pf; k++) M = fmaxf(M, smem[k * p.merge_blk + row * RF]);
+        for (int k = 0; k < pf; k++) M = fmaxf(M, pbuf[k * p.merge_blk + row * RF]);
         for (int k = pf; k < npieces; k++) M = fmaxf(M, rbase[k * rstride + row * RF]);
         const float wown = fast_exp2(mi - M);
         zi *= wown;
@@ -766,7 +773,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
             o[2 * b + 1][i] += f16_hi(hv[b]) * w;
           }
         };
-        for (int k = 0; k < pf; k++) fold(smem + k * p.merge_blk + row * RF);
+        for (int k = 0; k < pf; k++) fold(pbuf + k * p.merge_blk + row * RF);
         for (int k = pf; k < npieces; k++) fold(rbase + k * rstride + row * RF);
         }
       }
@@ -1085,7 +1092,7 @@ hipError_t launch_bf16(const AttnParams &p_in, const EntropyBatch *ent, hipStrea
     // LDS for the suffix kernel's prefetched partials: whole 1 KiB blocks per
     // piece, at most 16 KiB per wave (8 waves per CU then use 128 of 160 KiB).
     p.merge_blk = (p.G * kRecFloats<D> * 4 + 1023) / 1024 * 256;
-    const int fit = 16384 / (p.merge_blk * 4);
+    const int fit = (int)(kMergePrefetchBytes / (p.merge_blk * 4));
     p.merge_pf = p.nsplit < fit ? p.nsplit : fit;
   }
   const dim3 units(p.S * p.L * p.Hkv);
@@ -1121,8 +1128,13 @@ hipError_t launch_bf16(const AttnParams &p_in, const EntropyBatch *ent, hipStrea
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_cache_bf16<D, true, 2, 2>), units, dim3(64),
-                     (size_t)p.merge_pf * p.merge_blk * sizeof(float), stream, p, EntropyBatch{});
+  const size_t pre = (size_t)p.merge_pf * p.merge_blk * sizeof(float);
+  constexpr size_t ring = kl_ring<D, kKlTiles, kKlDepth>;
+  if constexpr (kSuffixKl)
+    hipLaunchKernelGGL((attn_cache_bf16<D, true, kKlTiles, kKlDepth, true>), units, dim3(64), ring + pre, stream, p,
+                       EntropyBatch{});
+  else
+    hipLaunchKernelGGL((attn_cache_bf16<D, true, 2, 2>), units, dim3(64), pre, stream, p, EntropyBatch{});
   return hipGetLastError();
 }
 
