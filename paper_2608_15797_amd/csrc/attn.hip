@@ -406,7 +406,16 @@ __device__ __forceinline__ void softmax_pv_core(float (&x)[TILES][4], RowState &
     for (int i = 0; i < 4; i++) cm = fmaxf(cm, x[t][i]);
   cm = fmaxf(cm, shfl_xor(cm, 16));
   cm = fmaxf(cm, shfl_xor(cm, 32));
-  const float mn = fmaxf(st.m, cm);
+  // LAZY (long streams): the reference st.m may trail the row's running
+  // maximum by up to kLagLog2 (probabilities up to 2^kLagLog2 before the
+  // normalisation, exact in float32 and bf16 alike), and moves only when a
+  // chunk exceeds it by more; the rescale of o then runs only on those rare
+  // chunks. With many rows per tile some row's maximum grows in most chunks,
+  // so the exact update rescaled (and moved the accumulators through VALU)
+  // almost every chunk. Otherwise the reference is the running maximum.
+  constexpr float kLagLog2 = 8.0f;
+  const bool need = LAZY ? cm > st.m + kLagLog2 : cm > st.m;
+  const float mn = need ? cm : st.m;
   const bool live = mn != kNegInf;
   const float alpha = live ? fast_exp2(st.m - mn) : 1.0f;
   float psum = 0.0f;
@@ -418,11 +427,9 @@ __device__ __forceinline__ void softmax_pv_core(float (&x)[TILES][4], RowState &
       psum += x[t][i];
     }
   st.zl = st.zl * alpha + psum;
-  const bool grew = mn > st.m;
+  const bool grew = need;
   st.m = mn;
-  // o rows are 4*g4 + i; their alphas live in lanes 4*g4 + i. LAZY (long
-  // streams): once the running maxima settle no row grows and the rescale is
-  // skipped.
+  // o rows are 4*g4 + i; their alphas live in lanes 4*g4 + i.
   if (!LAZY || __any(grew)) {
 #pragma unroll
     for (int i = 0; i < 4; i++) {
@@ -903,7 +910,7 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
       for (int rb = 0; rb < RB; rb++) {
         float x[TILES][4];
         chunk_logits<D, TILES>(c, qop[rb], x, c0, k1, g4, sl2, tail);
-        softmax_pv<D, TILES, false>(x, st[rb], o[rb], c.v, g4);
+        softmax_pv<D, TILES, true>(x, st[rb], o[rb], c.v, g4);
       }
     }
   };
