@@ -406,7 +406,7 @@ __device__ __forceinline__ void softmax_pv_core(float (&x)[TILES][4], RowState &
     for (int i = 0; i < 4; i++) cm = fmaxf(cm, x[t][i]);
   cm = fmaxf(cm, shfl_xor(cm, 16));
   cm = fmaxf(cm, shfl_xor(cm, 32));
-  // LAZY (long streams): the reference st.m may trail the row's running
+  // LAZY: the reference st.m may trail the row's running
   // maximum by up to kLagLog2 (probabilities up to 2^kLagLog2 before the
   // normalisation, exact in float32 and bf16 alike), and moves only when a
   // chunk exceeds it by more; the rescale of o then runs only on those rare
@@ -628,7 +628,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
         *reinterpret_cast<float4_t *>(xs + r16 * ldx + c0 + t * 16 + 4 * g4) =
             float4_t{x[t][0], x[t][1], x[t][2], x[t][3]};
     }
-    softmax_pv<D, TILES>(x, st, o, c.v, g4);
+    softmax_pv<D, TILES, true>(x, st, o, c.v, g4);
   };
 
   // The stored scores of window steps that accumulate are prefetched now,
@@ -671,7 +671,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
       float x[1][4];
       chunk_logits<D, 1>(cn, qop, x, 0, 1, g4, sl2, true);
       xnew = x[0][0];
-      softmax_pv<D, 1>(x, st, o, cn.v, g4);
+      softmax_pv<D, 1, true>(x, st, o, cn.v, g4);
     }
   };
   if constexpr (MERGE) {
