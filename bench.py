@@ -268,6 +268,32 @@ def calibration_copy(nbytes=1 << 30):
     torch.cuda.empty_cache()
 
 
+def sampler_marginal(dec, steps, reps=3):
+    """The sampler's marginal time in the decode step: for every step of
+    `steps`, the base-attention launch with the step's entropy rows and the
+    same launch drawing every row's next token too (temperature 0.8, top-k 20,
+    top-p 0.95), one after the other between timing events, `reps` times."""
+    import torch
+
+    from paper_2608_15797_amd import kvr
+    smp = kvr.Sampler(seed=2608)
+    timers = {}
+    for _ in range(reps):
+        for i in steps:
+            t = dec.T_prompt + i
+            si = dec.inputs(t)
+            sets = dec.logit_sets(si)
+            toks = [torch.empty(x.shape[0], dtype=torch.int32, device="cuda") for x in si.logits]
+            dec.base_attn(t, si, timers=timers, sets=sets)
+            dec.base_attn(t, si, timers=timers, sets=sets, sampler=smp, tokens=toks)
+    torch.cuda.synchronize()
+    avg = {k: sum(s.elapsed_time(e) for s, e in ev) / len(ev) * 1e3 for k, ev in timers.items()}
+    return dict(calls_per_kind=len(timers["base_attn_entropy"]),
+                entropy_call_us=round(avg["base_attn_entropy"], 2),
+                entropy_sample_call_us=round(avg["base_attn_entropy_sample"], 2),
+                marginal_us=round(avg["base_attn_entropy_sample"] - avg["base_attn_entropy"], 2))
+
+
 def sampler_cost(dec, wl, reps=50):
     """Per-call time of the entropy pass alone and with the fused sampler
     (temperature 0.8, top-k 20, top-p 0.95) on the workload's logit sets."""
@@ -509,6 +535,8 @@ def main():
     if rec is not None and "alg_bytes_per_dispatch" in rec:
         roof["traffic_alg_bytes_per_call"] = int(rec["alg_bytes_per_dispatch"])
     sampler = sampler_cost(dec, wl) if not args.no_instrument else None
+    if sampler is not None and dec.fuse_entropy:
+        sampler["in_decode_launch"] = sampler_marginal(dec, win)
     if sampler:
         log("[%s] sampler: %s" % (args.workload, json.dumps(sampler)))
     cpu = None

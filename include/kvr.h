@@ -329,6 +329,31 @@ int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const vo
                             const kvr_policy *policy, float *scores, const kvr_logit_set *sets, int32_t nsets,
                             hipStream_t stream);
 
+/*
+ * kvr_decode_attn_entropy_sample -- kvr_decode_attn_entropy, and the next
+ * token of every logit row drawn in the same launch (the sampler of
+ * kvr_logit_entropy_sample, Sec. 4.1 decoding setup: temperature, top-k,
+ * top-p): the step's decode attention, entropies, detector update and token
+ * draw in one pass over the cache and the logits.
+ *
+ *   sampler : the settings of kvr_sampler, applied to every set; required.
+ *   tokens  : host array of nsets pointers, tokens[k] an [R_k] int32 device
+ *             array receiving the sampled ids of set k (the draw for row r of
+ *             a set uses counter (step, r, 0, 0), as kvr_logit_entropy_sample
+ *             does for that set's rows alone).
+ * Arguments, results and errors otherwise as kvr_decode_attn_entropy; the
+ * tokens are those kvr_logit_entropy_sample draws from the same rows with the
+ * same settings (both take the k largest logits, ties to the lower id, and
+ * the same draw). Errors: KVR_EINVAL also for sampler settings out of range
+ * or a NULL tokens array or entry. Each row wave keeps its candidates in
+ * 2 KiB of the launch's LDS.
+ */
+int kvr_decode_attn_entropy_sample(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq,
+                                   float scale, const void *k_new, const void *v_new, const int32_t *new_pos,
+                                   void *out, const kvr_policy *policy, float *scores, const kvr_logit_set *sets,
+                                   int32_t nsets, const kvr_sampler *sampler, int32_t *const *tokens,
+                                   hipStream_t stream);
+
 /* Bytes of device scratch the library holds per GPU for
  * kvr_logit_entropy_batch_noalloc (the largest workspace it accepts). */
 #define KVR_ENTROPY_SCRATCH_BYTES ((size_t)1 << 20)

@@ -348,6 +348,14 @@ namespace {
 // Validates a batch and fills b (all but the workspace pointers); *need gets
 // the workspace size. With shapes_only, the sets' pointers are not checked
 // (the workspace size depends on the shapes alone).
+int check_sampler(const kvr_sampler *sampler) {
+  if (!(sampler->temperature > 0.f)) return fail(KVR_EINVAL, "temperature must be positive");
+  if (sampler->top_k < 1 || sampler->top_k > kvr::kTopKMax)
+    return fail(KVR_EINVAL, "top_k=%d is outside 1..%d", sampler->top_k, kvr::kTopKMax);
+  if (!(sampler->top_p > 0.f && sampler->top_p <= 1.f)) return fail(KVR_EINVAL, "top_p must lie in (0, 1]");
+  return KVR_OK;
+}
+
 int entropy_batch(const kvr_logit_set *sets, int32_t nsets, kvr::EntropyBatch *b, size_t *need,
                   bool shapes_only = false) {
   if (!sets) return fail(KVR_EINVAL, "sets is required");
@@ -441,11 +449,8 @@ int kvr_logit_entropy_sample(const void *logits, int32_t dtype, int32_t R, int32
   int st = entropy_params(logits, dtype, R, V, ld, inv_temp, H, det, &p);
   if (st) return st;
   if (!sampler || !tokens) return fail(KVR_EINVAL, "sampler and tokens are required");
-  if (!(sampler->temperature > 0.f)) return fail(KVR_EINVAL, "temperature must be positive");
-  if (sampler->top_k < 1 || sampler->top_k > kvr::kTopKMax)
-    return fail(KVR_EINVAL, "top_k=%d is outside 1..%d", sampler->top_k, kvr::kTopKMax);
-  if (!(sampler->top_p > 0.f && sampler->top_p <= 1.f))
-    return fail(KVR_EINVAL, "top_p must lie in (0, 1]");
+  st = check_sampler(sampler);
+  if (st) return st;
   p.top_k = sampler->top_k;
   p.inv_t = 1.0f / sampler->temperature;
   p.top_p = sampler->top_p;
@@ -460,6 +465,45 @@ int kvr_logit_entropy_sample(const void *logits, int32_t dtype, int32_t R, int32
 
 }  // extern "C"
 
+namespace {
+
+// Validates the arguments of the fused attention + entropy calls and fills p
+// and b (the sampler, when given, applies to every set).
+int fused_params(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq, float scale,
+                 const void *k_new, const void *v_new, const int32_t *new_pos, void *out, const kvr_policy *policy,
+                 float *scores, const kvr_logit_set *sets, int32_t nsets, const kvr_sampler *sampler,
+                 int32_t *const *tokens, kvr::AttnParams *p, kvr::EntropyBatch *b) {
+  int st = attn_params(cache, nullptr, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, nullptr, 0, p);
+  if (st) return st;
+  size_t need = 0;
+  st = entropy_batch(sets, nsets, b, &need);
+  if (st) return st;
+  const size_t esz = sets[0].dtype == KVR_F32 ? 4 : 2;
+  for (int k = 0; k < nsets; k++)
+    if (!aligned16(sets[k].logits) || ((size_t)sets[k].ld * esz) % 16 != 0)
+      return fail(KVR_EINVAL, "set %d: logit rows must start 16-byte aligned (logits and ld * element size)", k);
+  if ((double)b->row0[nsets] + (double)cache->S * cache->L * cache->Hkv > 2147483647.0)
+    return fail(KVR_EUNSUPPORTED, "logit rows plus attention units exceed the launch grid");
+  if (sampler) {
+    st = check_sampler(sampler);
+    if (st) return st;
+    if (!tokens) return fail(KVR_EINVAL, "tokens is required with a sampler");
+    for (int k = 0; k < nsets; k++) {
+      if (!tokens[k]) return fail(KVR_EINVAL, "set %d: tokens pointer is NULL", k);
+      kvr::EntropyParams &e = b->set[k];
+      e.top_k = sampler->top_k;
+      e.inv_t = 1.0f / sampler->temperature;
+      e.top_p = sampler->top_p;
+      e.seed = sampler->seed;
+      e.step = sampler->step;
+      e.tokens = tokens[k];
+    }
+  }
+  return KVR_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq, float scale,
@@ -467,20 +511,25 @@ int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const vo
                             const kvr_policy *policy, float *scores, const kvr_logit_set *sets, int32_t nsets,
                             hipStream_t stream) {
   kvr::AttnParams p;
-  int st = attn_params(cache, nullptr, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, nullptr, 0,
-                       &p);
-  if (st) return st;
   kvr::EntropyBatch b;
-  size_t need = 0;
-  st = entropy_batch(sets, nsets, &b, &need);
+  const int st = fused_params(cache, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, sets, nsets,
+                              nullptr, nullptr, &p, &b);
   if (st) return st;
-  const size_t esz = sets[0].dtype == KVR_F32 ? 4 : 2;
-  for (int k = 0; k < nsets; k++)
-    if (!aligned16(sets[k].logits) || ((size_t)sets[k].ld * esz) % 16 != 0)
-      return fail(KVR_EINVAL, "set %d: logit rows must start 16-byte aligned (logits and ld * element size)", k);
-  if ((double)b.row0[nsets] + (double)cache->S * cache->L * cache->Hkv > 2147483647.0)
-    return fail(KVR_EUNSUPPORTED, "logit rows plus attention units exceed the launch grid");
   return hip_status(kvr::launch_decode_attn(p, &b, stream), "kvr_decode_attn_entropy launch");
+}
+
+int kvr_decode_attn_entropy_sample(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq,
+                                   float scale, const void *k_new, const void *v_new, const int32_t *new_pos,
+                                   void *out, const kvr_policy *policy, float *scores, const kvr_logit_set *sets,
+                                   int32_t nsets, const kvr_sampler *sampler, int32_t *const *tokens,
+                                   hipStream_t stream) {
+  if (!sampler) return fail(KVR_EINVAL, "sampler is required");
+  kvr::AttnParams p;
+  kvr::EntropyBatch b;
+  const int st = fused_params(cache, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, sets, nsets,
+                              sampler, tokens, &p, &b);
+  if (st) return st;
+  return hip_status(kvr::launch_decode_attn(p, &b, stream), "kvr_decode_attn_entropy_sample launch");
 }
 
 }  // extern "C"

@@ -39,6 +39,7 @@
 #include <atomic>
 
 #include "entropy_common.h"
+#include "sampler_common.h"
 #include "kvr_device.h"
 #include "kvr_internal.h"
 
@@ -484,10 +485,12 @@ constexpr int kKlTiles = 2;
 constexpr int kKlDepth = 2;
 
 // LT (evicted cache only): 0, or the logit type of the step's entropy rows
-// computed in the same launch (1 = bfloat16, 2 = float32). The first
-// e.row0[e.nsets] workgroups of the grid are then one wave per logit row
-// (entropy_row_wave: the whole row, its entropy and detector update, no
-// partials); they are dispatched first and stream their rows while the
+// computed in the same launch (1 = bfloat16, 2 = float32; 3 and 4 the same
+// with the sampler). The first e.row0[e.nsets] workgroups of the grid are
+// then one wave per logit row (entropy_row_wave: the whole row, its entropy
+// and detector update, no partials; entropy_sample_row_wave also draws the
+// row's next token from its k best logits, using the launch's LDS for the
+// candidates); they are dispatched first and stream their rows while the
 // attention units run. The other workgroups are the attention units.
 template <int D, bool MERGE, int TILES, int DEPTH, bool KL = false, int LT = 0>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void attn_cache_bf16(AttnParams p,
@@ -503,10 +506,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
     const int rows = e.row0[e.nsets];
     if (unit < rows) {
       const int k = batch_set(e, unit);
+      uint64_t *cand = reinterpret_cast<uint64_t *>(smem);
       if constexpr (LT == 1)
         entropy_row_wave<bf16_t, 12>(e.set[k], unit - e.row0[k], threadIdx.x);
-      else
+      else if constexpr (LT == 2)
         entropy_row_wave<float, 6>(e.set[k], unit - e.row0[k], threadIdx.x);
+      else if constexpr (LT == 3)
+        entropy_sample_row_wave<bf16_t, 8>(e.set[k], unit - e.row0[k], threadIdx.x, cand);
+      else
+        entropy_sample_row_wave<float, 4>(e.set[k], unit - e.row0[k], threadIdx.x, cand);
       return;
     }
     unit -= rows;
@@ -1084,9 +1092,16 @@ void launch_own(const AttnParams &p, const EntropyBatch *e, size_t lds, hipStrea
   const int rows = e ? e->row0[e->nsets] : 0;
   const dim3 grid(rows + p.S * p.L * p.Hkv);
   const EntropyBatch none{};
+  const bool f32 = e && e->set[0].dtype == 0;
+  const bool sample = e && e->set[0].top_k > 0;
+  if (sample && lds < kSampleRowLds) lds = kSampleRowLds;  // the row waves' candidate buffers
   if (!e)
     hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 0>), grid, dim3(64), lds, stream, p, none);
-  else if (e->set[0].dtype == 0)
+  else if (sample && f32)
+    hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 4>), grid, dim3(64), lds, stream, p, *e);
+  else if (sample)
+    hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 3>), grid, dim3(64), lds, stream, p, *e);
+  else if (f32)
     hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 2>), grid, dim3(64), lds, stream, p, *e);
   else
     hipLaunchKernelGGL((attn_cache_bf16<D, false, TILES, DEPTH, KL, 1>), grid, dim3(64), lds, stream, p, *e);
@@ -1147,11 +1162,15 @@ hipError_t launch_bf16(const AttnParams &p_in, const EntropyBatch *ent, hipStrea
 
 // Whole logit rows, one wave per row, as a kernel of its own (the entropy
 // rows of a float32-cache launch, whose attention kernel has no such lanes).
-template <typename T>
+template <typename T, bool SAMPLE>
 __global__ __launch_bounds__(64) void entropy_rows_kernel(EntropyBatch e) {
+  extern __shared__ uint64_t cand[];
   const int g = blockIdx.x;
   const int k = batch_set(e, g);
-  entropy_row_wave<T, sizeof(T) == 2 ? 12 : 6>(e.set[k], g - e.row0[k], threadIdx.x);
+  if constexpr (SAMPLE)
+    entropy_sample_row_wave<T, sizeof(T) == 2 ? 8 : 4>(e.set[k], g - e.row0[k], threadIdx.x, cand);
+  else
+    entropy_row_wave<T, sizeof(T) == 2 ? 12 : 6>(e.set[k], g - e.row0[k], threadIdx.x);
 }
 
 }  // namespace
@@ -1224,8 +1243,15 @@ hipError_t launch_decode_attn(const AttnParams &p, const EntropyBatch *ent, hipS
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !ent) return e;
     const dim3 rows(ent->row0[ent->nsets]);
-    if (ent->set[0].dtype == 0) hipLaunchKernelGGL(entropy_rows_kernel<float>, rows, dim3(64), 0, stream, *ent);
-    else hipLaunchKernelGGL(entropy_rows_kernel<bf16_t>, rows, dim3(64), 0, stream, *ent);
+    const bool sample = ent->set[0].top_k > 0;
+    const size_t rlds = sample ? kSampleRowLds : 0;
+    if (ent->set[0].dtype == 0) {
+      if (sample) hipLaunchKernelGGL((entropy_rows_kernel<float, true>), rows, dim3(64), rlds, stream, *ent);
+      else hipLaunchKernelGGL((entropy_rows_kernel<float, false>), rows, dim3(64), 0, stream, *ent);
+    } else {
+      if (sample) hipLaunchKernelGGL((entropy_rows_kernel<bf16_t, true>), rows, dim3(64), rlds, stream, *ent);
+      else hipLaunchKernelGGL((entropy_rows_kernel<bf16_t, false>), rows, dim3(64), 0, stream, *ent);
+    }
     return hipGetLastError();
   }
   if (ent && p.P > 0) return hipErrorInvalidValue;

@@ -27,7 +27,7 @@ EXPORTS = ("kvr_strerror", "kvr_last_error", "kvr_decode_attn", "kvr_decode_attn
            "kvr_logit_entropy_workspace_size", "kvr_fork", "kvr_append",
            "kvr_logit_entropy_sample", "kvr_logit_entropy_sample_workspace_size",
            "kvr_redundancy_scores", "kvr_logit_entropy_batch", "kvr_logit_entropy_batch_workspace_size",
-           "kvr_logit_entropy_batch_noalloc", "kvr_decode_attn_entropy")
+           "kvr_logit_entropy_batch_noalloc", "kvr_decode_attn_entropy", "kvr_decode_attn_entropy_sample")
 
 
 class KvrError(RuntimeError):
@@ -99,6 +99,9 @@ def _load():
     lib.kvr_decode_attn_entropy.argtypes = [P(c_cache), vp, vp, i32, f32, vp, vp, vp, vp, P(c_policy), vp,
                                             P(c_logit_set), i32, vp]
     lib.kvr_decode_attn_entropy.restype = ctypes.c_int
+    lib.kvr_decode_attn_entropy_sample.argtypes = [P(c_cache), vp, vp, i32, f32, vp, vp, vp, vp, P(c_policy), vp,
+                                                   P(c_logit_set), i32, P(c_sampler), P(vp), vp]
+    lib.kvr_decode_attn_entropy_sample.restype = ctypes.c_int
     lib.kvr_logit_entropy_batch_noalloc.argtypes = [P(c_logit_set), i32, vp]
     lib.kvr_logit_entropy_batch_noalloc.restype = ctypes.c_int
     lib.kvr_logit_entropy_sample.argtypes = [vp, i32, i32, i32, i64, f32, vp, P(c_detector),
@@ -256,6 +259,26 @@ def decode_attn_entropy(cache: Cache, len_: torch.Tensor, q: torch.Tensor, out: 
                                      ctypes.byref(pol) if pol else None, _ptr(scores), arr, len(sets),
                                      _stream(stream))
     _check(rc, "kvr_decode_attn_entropy")
+
+
+def decode_attn_entropy_sample(cache: Cache, len_: torch.Tensor, q: torch.Tensor, out: torch.Tensor, scale: float,
+                               sets, sampler, tokens, k_new=None, v_new=None, new_pos=None,
+                               policy: Optional[Policy] = None, scores: Optional[torch.Tensor] = None,
+                               stream=None) -> None:
+    """kvr_decode_attn_entropy_sample: decode_attn_entropy plus the next token
+    of every row of every LogitSet; `tokens` holds one int32 tensor per set."""
+    cc = cache.c()
+    pol = policy.c() if policy is not None else None
+    for t in (len_, q, out, k_new, v_new, new_pos, scores, *tokens):
+        assert t is None or t.is_contiguous()
+    assert len(tokens) == len(sets)
+    arr = _logit_sets(sets)
+    tp = (ctypes.c_void_p * len(tokens))(*[t.data_ptr() for t in tokens])
+    rc = lib.kvr_decode_attn_entropy_sample(ctypes.byref(cc), _ptr(len_), _ptr(q), q.shape[2], float(scale),
+                                            _ptr(k_new), _ptr(v_new), _ptr(new_pos), _ptr(out),
+                                            ctypes.byref(pol) if pol else None, _ptr(scores), arr, len(sets),
+                                            ctypes.byref(sampler.c()), tp, _stream(stream))
+    _check(rc, "kvr_decode_attn_entropy_sample")
 
 
 def accumulate_scores(cache: Cache, len_: torch.Tensor, q_win: torch.Tensor, scale: float,

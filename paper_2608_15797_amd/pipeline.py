@@ -185,10 +185,18 @@ class Decoder:
             return True
         return False
 
-    def base_attn(self, t: int, si: StepInputs, stream=None, timers=None, only=None, sets=None) -> None:
+    def base_attn(self, t: int, si: StepInputs, stream=None, timers=None, only=None, sets=None, sampler=None,
+                  tokens=None) -> None:
         """The base-attention call of token t alone (append, attend, score),
-        with the entropies of `sets` in the same launch when given."""
-        if sets:
+        with the entropies of `sets` in the same launch when given, and with
+        `sampler` the next token of every row into `tokens` (one tensor per
+        set) as well."""
+        if sets and sampler is not None:
+            with _timer(timers, "base_attn_entropy_sample", stream, only):
+                kvr.decode_attn_entropy_sample(self.bcache, self.blen[t], si.bq, self.bout, self.bscale, sets,
+                                               sampler, tokens, k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t],
+                                               policy=self.policy, scores=self.scores, stream=stream)
+        elif sets:
             with _timer(timers, "base_attn_entropy", stream, only):
                 kvr.decode_attn_entropy(self.bcache, self.blen[t], si.bq, self.bout, self.bscale, sets,
                                         k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,

@@ -237,3 +237,30 @@ def test_decode_attn_entropy_rejects_on_host():
     arr[0] = kvr.c_logit_set(16, 1, 4, 1024, 1024, 1.0, 16, None)
     assert f(ctypes.byref(bad), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1, None) == -2
     assert f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 1, None) == -1
+
+
+def test_decode_attn_entropy_sample_rejects_on_host():
+    """The fused attention + entropy + sampler call checks what the fused
+    entropy call checks, the sampler settings and the tokens array."""
+    from paper_2608_15797_amd import kvr
+    f = kvr.lib.kvr_decode_attn_entropy_sample
+    c = _cache(kvr)
+    arr = (kvr.c_logit_set * 1)()
+    arr[0] = kvr.c_logit_set(16, 1, 4, 1024, 1024, 1.0, 16, None)
+    toks = (ctypes.c_void_p * 1)(16)
+    none = (ctypes.c_void_p * 1)(None)
+
+    def call(smp, t=toks):
+        return f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1,
+                 ctypes.byref(smp) if smp is not None else None, t, None)
+
+    assert call(None) == -1 and "sampler" in kvr.lib.kvr_last_error().decode()
+    for bad, msg in ((kvr.c_sampler(0.0, 20, 0.95, 0, 0), "temperature"), (kvr.c_sampler(0.8, 0, 0.95, 0, 0), "top_k"),
+                     (kvr.c_sampler(0.8, 65, 0.95, 0, 0), "top_k"), (kvr.c_sampler(0.8, 20, 0.0, 0, 0), "top_p"),
+                     (kvr.c_sampler(0.8, 20, 1.5, 0, 0), "top_p")):
+        assert call(bad) == -1 and msg in kvr.lib.kvr_last_error().decode()
+    good = kvr.c_sampler(0.8, 20, 0.95, 0, 0)
+    assert call(good, None) == -1 and "tokens" in kvr.lib.kvr_last_error().decode()
+    assert call(good, none) == -1 and "tokens" in kvr.lib.kvr_last_error().decode()
+    arr[0] = kvr.c_logit_set(16, 1, 4, 1001, 1001, 1.0, 16, None)  # rows not 16-byte aligned
+    assert call(good) == -1 and "aligned" in kvr.lib.kvr_last_error().decode()

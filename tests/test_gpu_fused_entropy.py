@@ -134,3 +134,75 @@ def test_decode_attn_entropy_rejects_unaligned_rows():
     with pytest.raises(k.KvrError) as e:
         k.decode_attn_entropy(cache, lent, q, out, 1.0, [k.LogitSet(x, torch.empty(4, device=DEV))])
     assert e.value.status == -1 and "aligned" in str(e.value)
+
+
+SAMPLE_CASES = [
+    # cache (S, L, Hkv, G, D, B, W, buffer, dtype), logit dtype, sets [(R, V, ld, kind)], sampler (T, k, p, seed, step)
+    ((4, 2, 4, 7, 128, 64, 32, 64, torch.bfloat16), torch.bfloat16,
+     [(16, 152064, 152064, "boosted"), (9, 151936, 152000, "ties")], (0.8, 20, 0.95, 1234, 7)),
+    ((3, 2, 2, 8, 128, 16, 4, 8, torch.bfloat16), torch.float32,
+     [(5, 1023, 1024, 2.0), (3, 5, 8, 1.0), (2, 8, 8, "flat")], (1.0, 64, 1.0, 9, 0)),
+    ((1, 1, 1, 4, 64, 16, 8, 16, torch.float32), torch.bfloat16, [(4, 1024, 1024, 2.0)], (0.5, 1, 0.5, 3, 2)),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(SAMPLE_CASES)))
+def test_decode_attn_entropy_sample_matches_separate_calls(ci):
+    """kvr_decode_attn_entropy_sample: attention bit for bit as
+    kvr_decode_attn, entropies within 1e-4 of the oracle, and every set's
+    tokens identical to kvr_logit_entropy_sample's on the same rows and
+    settings (same k best logits, same draw), which in turn follow the
+    oracle sampler (oracle/sampler.py) as in test_gpu_sampler."""
+    from paper_2608_15797_amd import kvr as k
+    from test_gpu_sampler import _check_tokens, _logits
+    (S, L, Hkv, G, D, B, W, buffer, dt), ldt, specs, (T, topk, topp, seed, step) = SAMPLE_CASES[ci]
+    say("case", ci, "cache", SAMPLE_CASES[ci][0], "logits", ldt, "sets", specs)
+    Hq = Hkv * G
+    cap = B + buffer + 1
+    g = torch.Generator().manual_seed(5151 + ci)
+    scale = 1.0 / math.sqrt(D)
+    K = _randn((S, L, Hkv, cap, D), g, dt)
+    V = _randn((S, L, Hkv, cap, D), g, dt)
+    pos = torch.randint(0, 999, (S, L, Hkv, cap), generator=g, dtype=torch.int32)
+    pol = k.Policy(B, W, buffer)
+    smp = k.Sampler(temperature=T, top_k=topk, top_p=topp, seed=seed, step=step)
+    xs = [_logits(R, V_, ld, ldt, kind, 77 + j) for j, (R, V_, ld, kind) in enumerate(specs)]
+    lens = [min(cap, B + buffer + 2 - W + s) for s in range(S)]
+    lent = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    q = _randn((S, L, Hq, D), g, dt).to(DEV)
+    kn = _randn((S, L, Hkv, D), g, dt).to(DEV)
+    vn = _randn((S, L, Hkv, D), g, dt).to(DEV)
+    npos = (torch.arange(S, dtype=torch.int32) + 2000).to(DEV)
+    sc0 = torch.rand((S, L, Hkv, cap), generator=g)
+    ca = k.Cache(K.to(DEV), V.to(DEV), pos.to(DEV))
+    cb = k.Cache(K.to(DEV), V.to(DEV), pos.to(DEV))
+    sa, sb = sc0.to(DEV), sc0.to(DEV)
+    oa = torch.empty((S, L, Hq, D), dtype=dt, device=DEV)
+    ob = torch.empty_like(oa)
+    k.decode_attn(ca, lent, q, oa, scale, k_new=kn, v_new=vn, new_pos=npos, policy=pol, scores=sa)
+    ref_tok = []
+    for x, (R, V_, ld, kind) in zip(xs, specs):
+        H = torch.empty(R, device=DEV)
+        tok = torch.full((R,), -7, dtype=torch.int32, device=DEV)
+        ws = torch.empty(max(k.logit_entropy_sample_workspace_size(R, V_, topk), 16) // 4 + 4, device=DEV)
+        k.logit_entropy_sample(x.to(DEV), H, tok, smp, V=V_, workspace=ws)
+        ref_tok.append(tok)
+    sets = [k.LogitSet(x.to(DEV), torch.full((x.shape[0],), float("nan"), device=DEV), V_, 1.0)
+            for x, (R, V_, ld, kind) in zip(xs, specs)]
+    toks = [torch.full((x.shape[0],), -7, dtype=torch.int32, device=DEV) for x in xs]
+    k.decode_attn_entropy_sample(cb, lent, q, ob, scale, sets, smp, toks, k_new=kn, v_new=vn, new_pos=npos,
+                                 policy=pol, scores=sb)
+    torch.cuda.synchronize()
+    bits = (lambda t: t.cpu().view(torch.int16)) if dt == torch.bfloat16 else (lambda t: t.cpu())
+    assert torch.equal(bits(oa), bits(ob))
+    assert torch.equal(sa.cpu(), sb.cpu())
+    for t in ("k", "v"):
+        assert torch.equal(bits(getattr(ca, t)), bits(getattr(cb, t)))
+    for j, (x, (R, V_, ld, kind)) in enumerate(zip(xs, specs)):
+        got = toks[j].cpu().numpy()
+        assert (got == ref_tok[j].cpu().numpy()).all(), (j, got, ref_tok[j].cpu().numpy())
+        exact, loose = _check_tokens(host(x), V_, smp, got)
+        href = oracle.entropy(host(x), V=V_)
+        d = np.abs(sets[j].H.cpu().double().numpy() - href).max()
+        say("  set", j, "tokens", got[:8].tolist(), "oracle-exact", exact, "near-threshold", loose, "H err", d)
+        assert d <= 1e-4
