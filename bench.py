@@ -28,10 +28,11 @@ prompt is decoded (teacher-forced) first; then the warmup steps, then exactly
 K timed steps between two synchronisations, with HIP events on the launch
 stream around each call of the dominant call (the roofline's kernel time).
 A replay of the same K step indices brackets every call with events for the
-per-call table. When the entropies ride in the base-attention launch, a second
-pass runs, at every step of the window, the fused call, base attention alone
-and the entropy call alone, one after the other, three times: the difference
-between the fused call and base attention alone is entropy's marginal time
+per-call table. The entropies ride in the base-attention launch (in the
+helper's context launch when there is no base model); a second pass runs, at
+every step of the window, the fused call, the same attention call alone and
+the entropy call alone, one after the other, three times: the difference
+between the fused call and the attention alone is entropy's marginal time
 ("entropy_marginal"). Unless the window already is one, a whole
 cycle is then timed and replayed the same way and reported under "cycle".
 
@@ -122,25 +123,31 @@ def per_call(wl, dec, steps):
 
 
 def entropy_marginal(wl, dec, steps, reps=3):
-    """Entropy's marginal time in the fused base-attention launch: for every
-    step of `steps`, the fused call, base attention alone and the entropy
+    """Entropy's marginal time in the fused attention launch (base attention,
+    or the helper's context launch when there is no base model): for every
+    step of `steps`, the fused call, the same attention alone and the entropy
     call alone, one after the other, each between timing events, `reps`
     times. marginal = mean(fused) - mean(alone)."""
     import torch
+    fused, alone = ("base_attn_entropy", "base_attn") if wl.base else ("helper_attn_entropy", "helper_attn")
     timers = {}
     for _ in range(reps):
         for i in steps:
             t = dec.T_prompt + i
             si = dec.inputs(t)
-            dec.base_attn(t, si, timers=timers, sets=dec.logit_sets(si))
-            dec.base_attn(t, si, timers=timers)
+            if wl.base:
+                dec.base_attn(t, si, timers=timers, sets=dec.logit_sets(si))
+                dec.base_attn(t, si, timers=timers)
+            else:
+                dec.helper_token(i, si, timers=timers, sets=dec.logit_sets(si))
+                dec.helper_token(i, si, timers=timers)
             dec.entropy(si, timers=timers)
     torch.cuda.synchronize()
     avg = {k: sum(s.elapsed_time(e) for s, e in ev) / len(ev) * 1e3 for k, ev in timers.items()}
     eb = acc.entropy_bytes(wl)
-    mus = avg["base_attn_entropy"] - avg["base_attn"]
-    return dict(calls_per_kind=len(timers["base_attn"]), fused_call_us=round(avg["base_attn_entropy"], 2),
-                base_attn_alone_us=round(avg["base_attn"], 2), marginal_us=round(mus, 2),
+    mus = avg[fused] - avg[alone]
+    return dict(call=fused, calls_per_kind=len(timers[alone]), fused_call_us=round(avg[fused], 2),
+                attn_alone_us=round(avg[alone], 2), marginal_us=round(mus, 2),
                 separate_call_us=round(avg["entropy"], 2), bytes_per_step=eb,
                 GBps=round(eb / (mus * 1e-6) / 1e9, 1) if mus > 0 else None,
                 frac=round(eb / (mus * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4) if mus > 0 else None,
@@ -535,7 +542,7 @@ def main():
     if rec is not None and "alg_bytes_per_dispatch" in rec:
         roof["traffic_alg_bytes_per_call"] = int(rec["alg_bytes_per_dispatch"])
     sampler = sampler_cost(dec, wl) if not args.no_instrument else None
-    if sampler is not None and dec.fuse_entropy:
+    if sampler is not None and dec.fuse_entropy and wl.base:
         sampler["in_decode_launch"] = sampler_marginal(dec, win)
     if sampler:
         log("[%s] sampler: %s" % (args.workload, json.dumps(sampler)))

@@ -308,26 +308,33 @@ int kvr_logit_entropy_batch(const kvr_logit_set *sets, int32_t nsets, void *work
 size_t kvr_logit_entropy_batch_workspace_size(const kvr_logit_set *sets, int32_t nsets);
 
 /*
- * kvr_decode_attn_entropy -- kvr_decode_attn over the sequences' own caches
- * (no prefix) and kvr_logit_entropy_batch over the step's logit sets in one
- * launch: the detector's entropies are by-products of the decode step (App.
- * C: the signals add negligible cost), so their rows are read while the
- * attention units stream their caches (Eq. (1) third line; Eq. (4)).
+ * kvr_decode_attn_entropy -- kvr_decode_attn and kvr_logit_entropy_batch over
+ * the step's logit sets in one launch: the detector's entropies are
+ * by-products of the decode step (App. C: the signals add negligible cost),
+ * so their rows are read while the attention waves stream their caches (Eq.
+ * (1) third line; Sec. 3.1; Eq. (4)).
  *
- * Arguments, results and errors are those of kvr_decode_attn (with prefix =
- * NULL and no workspace) and of kvr_logit_entropy_batch (sets, nsets), with
- * one more requirement: every set's rows start 16-byte aligned (logits and
- * ld * element size), KVR_EINVAL otherwise. Each logit row is reduced whole
- * by one wavefront of the launch, so no workspace is needed. The attention
- * outputs and scores are bit for bit those of kvr_decode_attn; the entropies
- * agree with kvr_logit_entropy_batch to float32 rounding (different summation
- * order). For a float32 cache the entropy rows run as a second kernel on the
- * same stream.
+ * Arguments, results and errors are those of kvr_decode_attn (cache, prefix,
+ * ..., workspace) and of kvr_logit_entropy_batch (sets, nsets), with one more
+ * requirement: every set's rows start 16-byte aligned (logits and ld *
+ * element size), KVR_EINVAL otherwise. Each logit row is reduced whole by one
+ * wavefront of the launch, so the rows need no workspace.
+ *   Without a prefix the rows ride in the own-cache launch, and the attention
+ *   outputs and scores are bit for bit those of kvr_decode_attn.
+ *   With a prefix (bfloat16 cache) they ride in the context launch, whose
+ *   split plan gives their wavefronts slots of their own (at most half of
+ *   the chip's), so the context is cut at other points than kvr_decode_attn
+ *   cuts it: the outputs agree with kvr_decode_attn's to the rounding of
+ *   the split partials. The workspace size is kvr_decode_attn_workspace_size
+ *   (cache, prefix, Hq), which covers this plan.
+ * The entropies agree with kvr_logit_entropy_batch to float32 rounding
+ * (different summation order). For a float32 cache the entropy rows run as
+ * a second kernel on the same stream.
  */
-int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq, float scale,
-                            const void *k_new, const void *v_new, const int32_t *new_pos, void *out,
-                            const kvr_policy *policy, float *scores, const kvr_logit_set *sets, int32_t nsets,
-                            hipStream_t stream);
+int kvr_decode_attn_entropy(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len, const void *q,
+                            int32_t Hq, float scale, const void *k_new, const void *v_new, const int32_t *new_pos,
+                            void *out, const kvr_policy *policy, float *scores, void *workspace,
+                            size_t workspace_bytes, const kvr_logit_set *sets, int32_t nsets, hipStream_t stream);
 
 /*
  * kvr_decode_attn_entropy_sample -- kvr_decode_attn_entropy, and the next
@@ -346,11 +353,12 @@ int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const vo
  * same settings (both take the k largest logits, ties to the lower id, and
  * the same draw). Errors: KVR_EINVAL also for sampler settings out of range
  * or a NULL tokens array or entry. Each row wave keeps its candidates in
- * 2 KiB of the launch's LDS.
+ * 2 KiB of its LDS.
  */
-int kvr_decode_attn_entropy_sample(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq,
-                                   float scale, const void *k_new, const void *v_new, const int32_t *new_pos,
-                                   void *out, const kvr_policy *policy, float *scores, const kvr_logit_set *sets,
+int kvr_decode_attn_entropy_sample(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len,
+                                   const void *q, int32_t Hq, float scale, const void *k_new, const void *v_new,
+                                   const int32_t *new_pos, void *out, const kvr_policy *policy, float *scores,
+                                   void *workspace, size_t workspace_bytes, const kvr_logit_set *sets,
                                    int32_t nsets, const kvr_sampler *sampler, int32_t *const *tokens,
                                    hipStream_t stream);
 

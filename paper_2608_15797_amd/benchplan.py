@@ -33,8 +33,9 @@ class Schedule:
     def __init__(self, wl, horizon, fuse_entropy=None):
         self.wl = wl
         b, h = wl.base, wl.helper
-        # As the decode driver: entropies in the base-attention launch when there is one.
-        self.fuse_entropy = bool(b and wl.logits) if fuse_entropy is None else fuse_entropy
+        # As the decode driver: entropies in the base-attention launch, or in
+        # the helper's context launch when there is no base model.
+        self.fuse_entropy = bool(wl.logits) if fuse_entropy is None else fuse_entropy
         self.T_prompt = b.prompt if b else 0
         self.blen_host = base_length_schedule(self.T_prompt + horizon, b.B, b.buffer) if b else None
         self.hlen_host = helper_suffix_schedule(horizon, h.scap) if h else None
@@ -110,9 +111,10 @@ def window_stats(wl, sch, s0, K):
 def step_bytes(wl, dec, i, moved_rows=None):
     """Algorithmic bytes of decode step i by call name. moved_rows: kept rows
     per head that change slot at an eviction, on average (None = all B, the
-    upper bound). When the decoder computes the entropies in the base-attention
-    launch (dec.fuse_entropy), that call is "base_attn_entropy" and carries
-    the logit bytes too."""
+    upper bound). When the decoder computes the entropies inside an attention
+    launch (dec.fuse_entropy), that call is "base_attn_entropy" (with a base
+    model) or "helper_attn_entropy" (helper only) and carries the logit bytes
+    too."""
     out = {}
     fused = getattr(dec, "fuse_entropy", False) and bool(wl.logits)
     if wl.base:
@@ -125,7 +127,10 @@ def step_bytes(wl, dec, i, moved_rows=None):
         if n > b.B + b.buffer:
             out["evict"] = acc.evict_bytes(wl, n, moved_rows)
     if wl.helper:
-        out["helper_attn"] = acc.helper_attn_bytes(wl, dec.hlen_host[i])
+        if fused and not wl.base:
+            out["helper_attn_entropy"] = acc.helper_attn_bytes(wl, dec.hlen_host[i]) + acc.entropy_bytes(wl)
+        else:
+            out["helper_attn"] = acc.helper_attn_bytes(wl, dec.hlen_host[i])
     if wl.logits and not fused:
         out["entropy"] = acc.entropy_bytes(wl)  # every logit set, one batched call
     return out

@@ -83,7 +83,7 @@ size_t kvr_decode_attn_workspace_size(const kvr_cache *cache, const kvr_prefix *
   if (cache->Hkv <= 0 || Hq <= 0 || Hq % cache->Hkv != 0 || cache->S % prefix->P != 0) return 0;
   int ns = 1, span = 1, nw = 1;
   const int rows = (cache->S / prefix->P) * (Hq / cache->Hkv);
-  kvr::plan_prefix_splits(cache->D, prefix->P, cache->L, cache->Hkv, prefix->plen, rows, &ns, &span, &nw);
+  kvr::plan_prefix_splits(cache->D, prefix->P, cache->L, cache->Hkv, prefix->plen, rows, 0, &ns, &span, &nw);
   return kvr::attn_workspace_bytes(cache->S, cache->L, Hq, cache->D, ns);
 }
 
@@ -91,10 +91,11 @@ size_t kvr_decode_attn_workspace_size(const kvr_cache *cache, const kvr_prefix *
 
 namespace {
 
-// Validates the arguments of kvr_decode_attn and fills p.
+// Validates the arguments of kvr_decode_attn and fills p; ent_rows logit rows
+// ride in the same launch (0: none).
 int attn_params(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len, const void *q, int32_t Hq,
                 float scale, const void *k_new, const void *v_new, const int32_t *new_pos, void *out,
-                const kvr_policy *policy, float *scores, void *workspace, size_t workspace_bytes,
+                const kvr_policy *policy, float *scores, void *workspace, size_t workspace_bytes, int ent_rows,
                 kvr::AttnParams *pp) {
   kvr::AttnParams &p = *pp;
   int G = 0;
@@ -138,7 +139,7 @@ int attn_params(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t 
     if (cache->dtype == KVR_BF16) {
       if (p.C * G > 64)
         return fail(KVR_EUNSUPPORTED, "%d candidates x %d heads per shared prefix exceeds 64 rows", p.C, G);
-      kvr::plan_prefix_splits(p.D, p.P, p.L, p.Hkv, p.plen, p.C * G, &p.nsplit, &p.span, &p.nwaves);
+      kvr::plan_prefix_splits(p.D, p.P, p.L, p.Hkv, p.plen, p.C * G, ent_rows, &p.nsplit, &p.span, &p.nwaves);
       const size_t need = kvr::attn_workspace_bytes(p.S, p.L, Hq, p.D, p.nsplit);
       if (!workspace || workspace_bytes < need)
         return fail(KVR_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
@@ -164,7 +165,7 @@ int kvr_decode_attn(const kvr_cache *cache, const kvr_prefix *prefix, const int3
                     void *workspace, size_t workspace_bytes, hipStream_t stream) {
   kvr::AttnParams p;
   const int st = attn_params(cache, prefix, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores,
-                             workspace, workspace_bytes, &p);
+                             workspace, workspace_bytes, 0, &p);
   if (st) return st;
   return hip_status(kvr::launch_decode_attn(p, nullptr, stream), "kvr_decode_attn launch");
 }
@@ -469,14 +470,16 @@ namespace {
 
 // Validates the arguments of the fused attention + entropy calls and fills p
 // and b (the sampler, when given, applies to every set).
-int fused_params(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq, float scale,
-                 const void *k_new, const void *v_new, const int32_t *new_pos, void *out, const kvr_policy *policy,
-                 float *scores, const kvr_logit_set *sets, int32_t nsets, const kvr_sampler *sampler,
-                 int32_t *const *tokens, kvr::AttnParams *p, kvr::EntropyBatch *b) {
-  int st = attn_params(cache, nullptr, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, nullptr, 0, p);
-  if (st) return st;
+int fused_params(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len, const void *q, int32_t Hq,
+                 float scale, const void *k_new, const void *v_new, const int32_t *new_pos, void *out,
+                 const kvr_policy *policy, float *scores, void *workspace, size_t workspace_bytes,
+                 const kvr_logit_set *sets, int32_t nsets, const kvr_sampler *sampler, int32_t *const *tokens,
+                 kvr::AttnParams *p, kvr::EntropyBatch *b) {
   size_t need = 0;
-  st = entropy_batch(sets, nsets, b, &need);
+  int st = entropy_batch(sets, nsets, b, &need);
+  if (st) return st;
+  st = attn_params(cache, prefix, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, workspace,
+                   workspace_bytes, b->row0[nsets], p);
   if (st) return st;
   const size_t esz = sets[0].dtype == KVR_F32 ? 4 : 2;
   for (int k = 0; k < nsets; k++)
@@ -506,28 +509,29 @@ int fused_params(const kvr_cache *cache, const int32_t *len, const void *q, int3
 
 extern "C" {
 
-int kvr_decode_attn_entropy(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq, float scale,
-                            const void *k_new, const void *v_new, const int32_t *new_pos, void *out,
-                            const kvr_policy *policy, float *scores, const kvr_logit_set *sets, int32_t nsets,
-                            hipStream_t stream) {
+int kvr_decode_attn_entropy(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len, const void *q,
+                            int32_t Hq, float scale, const void *k_new, const void *v_new, const int32_t *new_pos,
+                            void *out, const kvr_policy *policy, float *scores, void *workspace,
+                            size_t workspace_bytes, const kvr_logit_set *sets, int32_t nsets, hipStream_t stream) {
   kvr::AttnParams p;
   kvr::EntropyBatch b;
-  const int st = fused_params(cache, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, sets, nsets,
-                              nullptr, nullptr, &p, &b);
+  const int st = fused_params(cache, prefix, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores,
+                              workspace, workspace_bytes, sets, nsets, nullptr, nullptr, &p, &b);
   if (st) return st;
   return hip_status(kvr::launch_decode_attn(p, &b, stream), "kvr_decode_attn_entropy launch");
 }
 
-int kvr_decode_attn_entropy_sample(const kvr_cache *cache, const int32_t *len, const void *q, int32_t Hq,
-                                   float scale, const void *k_new, const void *v_new, const int32_t *new_pos,
-                                   void *out, const kvr_policy *policy, float *scores, const kvr_logit_set *sets,
+int kvr_decode_attn_entropy_sample(const kvr_cache *cache, const kvr_prefix *prefix, const int32_t *len,
+                                   const void *q, int32_t Hq, float scale, const void *k_new, const void *v_new,
+                                   const int32_t *new_pos, void *out, const kvr_policy *policy, float *scores,
+                                   void *workspace, size_t workspace_bytes, const kvr_logit_set *sets,
                                    int32_t nsets, const kvr_sampler *sampler, int32_t *const *tokens,
                                    hipStream_t stream) {
   if (!sampler) return fail(KVR_EINVAL, "sampler is required");
   kvr::AttnParams p;
   kvr::EntropyBatch b;
-  const int st = fused_params(cache, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores, sets, nsets,
-                              sampler, tokens, &p, &b);
+  const int st = fused_params(cache, prefix, len, q, Hq, scale, k_new, v_new, new_pos, out, policy, scores,
+                              workspace, workspace_bytes, sets, nsets, sampler, tokens, &p, &b);
   if (st) return st;
   return hip_status(kvr::launch_decode_attn(p, &b, stream), "kvr_decode_attn_entropy_sample launch");
 }

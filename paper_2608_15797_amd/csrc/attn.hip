@@ -280,6 +280,8 @@ __device__ __forceinline__ void load_chunk_lds(VChunk<D, TILES> &c, char *slot, 
 #pragma unroll
   for (int I = 0; I < KLOffsets<D, TILES>::KI; I++)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(K, (lds_void_t *)(slot + I * 1024), 16, off.k[I], 0, 0, 0);
+#else
+  (void)K;  // the host pass has no buffer-to-LDS loads
 #endif
 #pragma unroll
   for (int t = 0; t < TILES; t++)
@@ -837,26 +839,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void at
 // KV head, key) space one unit segment at a time; RB row blocks of 16 rows
 // hold the C*G query rows (candidate c, head g) sharing the prefix, so each
 // prefix byte is read once per step for all of them. Same double-buffered
-// chunk stream as the own-cache kernel.
+// chunk stream as the own-cache kernel. `wave` is the wave's index in the
+// plan (its span is keys [wave * span, (wave + 1) * span)).
+//
+// deferred: records of the wave's first segment when more follow,
+// [rows][4 + D/2] floats in LDS, written to the workspace once the span is
+// done. Stores to HBM in the middle of a wave's read stream cost far more
+// than their bytes (measured: about 6% of the kernel's time), so every record
+// store waits for the end of the wave.
 template <int D, int RB, int TILES, int DEPTH>
-__global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
+__device__ __forceinline__ void prefix_wave(const AttnParams &p, const int wave, float *deferred) {
   constexpr int CH = 16 * TILES;
   constexpr int NB = Geo<D>::NB;
   constexpr uint32_t ROW = D * 2;
   const long total = (long)p.P * p.L * p.Hkv * p.plen;
-  const long g0 = (long)blockIdx.x * p.span;
+  const long g0 = (long)wave * p.span;
   const long g1 = g0 + p.span < total ? g0 + p.span : total;
   const int lane = threadIdx.x;
   const int r16 = lane & 15;
   const int g4 = lane >> 4;
   const int G = p.G;
   const int rows = p.C * G;
-  // Records of the wave's first segment when more follow: [rows][4 + D/2]
-  // floats in LDS, written to the workspace once the span is done. Stores
-  // to HBM in the middle of a wave's read stream cost far more than their
-  // bytes (measured: about 6% of the kernel's time), so every record store
-  // waits for the end of the wave.
-  extern __shared__ float deferred[];
   int dunit = -1, dsplit = 0;
 
   // This wave's keys [g0, g1) of the flattened (unit, key) space, one segment
@@ -866,7 +869,7 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
   const int unit = (int)(g / p.plen);  // ((pp * L) + l) * Hkv + h
   const int k0 = (int)(g - (long)unit * p.plen);
   const int k1 = (int)((long)p.plen < k0 + (g1 - g) ? (long)p.plen : k0 + (g1 - g));
-  const int split = blockIdx.x - (int)((long)unit * p.plen / p.span);  // piece index within the unit
+  const int split = wave - (int)((long)unit * p.plen / p.span);  // piece index within the unit
   g += k1 - k0;
   const int h = unit % p.Hkv;
   const int pl = unit / p.Hkv;
@@ -987,6 +990,44 @@ __global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
   }
 }
 
+template <int D, int RB, int TILES, int DEPTH>
+__global__ __launch_bounds__(64) void attn_prefix_bf16(AttnParams p) {
+  extern __shared__ float deferred[];
+  prefix_wave<D, RB, TILES, DEPTH>(p, blockIdx.x, deferred);
+}
+
+// One logit row of the batch (global row g) by one wave, the variant picked at
+// run time from the batch's logit type and sampler; cand: kSampleRowLds bytes
+// of LDS owned by the wave.
+__device__ __forceinline__ void entropy_row_any(const EntropyBatch &e, int g, int lane, uint64_t *cand) {
+  const int k = batch_set(e, g);
+  const EntropyParams &s = e.set[k];
+  const int row = g - e.row0[k];
+  if (s.top_k > 0) {
+    if (s.dtype == 0) entropy_sample_row_wave<float, 4>(s, row, lane, cand);
+    else entropy_sample_row_wave<bf16_t, 8>(s, row, lane, cand);
+  } else {
+    if (s.dtype == 0) entropy_row_wave<float, 6>(s, row, lane);
+    else entropy_row_wave<bf16_t, 12>(s, row, lane);
+  }
+}
+
+// The prefix kernel with the step's logit rows in front: the first
+// e.row0[e.nsets] workgroups are one wave per row (entropy, detector update
+// and, with a sampler, the token draw), dispatched first so that they stream
+// their rows beside the context waves; the plan then has that many fewer
+// context waves, so that both fit on the chip in one round.
+template <int D, int RB, int TILES, int DEPTH>
+__global__ __launch_bounds__(64) void attn_prefix_rows_bf16(AttnParams p, EntropyBatch e) {
+  extern __shared__ float deferred[];
+  const int rows = e.row0[e.nsets];
+  if ((int)blockIdx.x < rows) {
+    entropy_row_any(e, blockIdx.x, threadIdx.x, reinterpret_cast<uint64_t *>(deferred));
+    return;
+  }
+  prefix_wave<D, RB, TILES, DEPTH>(p, blockIdx.x - rows, deferred);
+}
+
 // ---------------------------------------------------------------------------
 // float32 path: one wave per (sequence, layer, KV head), VALU arithmetic.
 // LDS: q rows [G][D], logits [G][nt_max], stats [2][16].
@@ -1079,10 +1120,23 @@ __global__ __launch_bounds__(64) void attn_f32(AttnParams p, int nt_max) {
   }
 }
 
-// LDS of a context-kernel wave: the deferred records of RB * 16 rows.
+// LDS of a context-kernel wave: the deferred records of RB * 16 rows. A
+// logit-row wave of the same launch uses the first kSampleRowLds bytes of it.
 template <int D>
 size_t prefix_lds_bytes(int rb) {
   return (size_t)rb * 16 * kRecFloats<D> * sizeof(float);
+}
+static_assert(16 * kRecFloats<64> * sizeof(float) >= kSampleRowLds, "row waves fit the context kernel's LDS");
+
+// The context kernel, with the entropy rows of `e` (nullptr: none) in front.
+template <int D, int RB, int TILES>
+void launch_prefix(const AttnParams &p, const EntropyBatch *e, hipStream_t stream) {
+  const size_t lds = prefix_lds_bytes<D>(RB);
+  if (e)
+    hipLaunchKernelGGL((attn_prefix_rows_bf16<D, RB, TILES, 2>), dim3(e->row0[e->nsets] + p.nwaves), dim3(64), lds,
+                       stream, p, *e);
+  else
+    hipLaunchKernelGGL((attn_prefix_bf16<D, RB, TILES, 2>), dim3(p.nwaves), dim3(64), lds, stream, p);
 }
 
 // The evicted-cache kernel with the entropy rows of `e` (nullptr: none) in
@@ -1137,15 +1191,13 @@ hipError_t launch_bf16(const AttnParams &p_in, const EntropyBatch *ent, hipStrea
     }
     return hipGetLastError();
   }
-  // Context splits first; the suffix kernel then merges their partials.
-  const int rb = (p.C * p.G + 15) / 16;
-  const dim3 gridA(p.nwaves);
-  const size_t lds = prefix_lds_bytes<D>(rb);
-  switch (rb) {
-    case 1: hipLaunchKernelGGL((attn_prefix_bf16<D, 1, 2, 2>), gridA, dim3(64), lds, stream, p); break;
-    case 2: hipLaunchKernelGGL((attn_prefix_bf16<D, 2, 2, 2>), gridA, dim3(64), lds, stream, p); break;
-    case 3: hipLaunchKernelGGL((attn_prefix_bf16<D, 3, 1, 2>), gridA, dim3(64), lds, stream, p); break;
-    case 4: hipLaunchKernelGGL((attn_prefix_bf16<D, 4, 1, 2>), gridA, dim3(64), lds, stream, p); break;
+  // Context splits first (with the logit rows, if any); the suffix kernel
+  // then merges their partials.
+  switch ((p.C * p.G + 15) / 16) {
+    case 1: launch_prefix<D, 1, 2>(p, ent, stream); break;
+    case 2: launch_prefix<D, 2, 2>(p, ent, stream); break;
+    case 3: launch_prefix<D, 3, 1>(p, ent, stream); break;
+    case 4: launch_prefix<D, 4, 1>(p, ent, stream); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
@@ -1181,9 +1233,10 @@ size_t f32_attn_lds_bytes(int G, int D, int plen, int cap) {
 
 namespace {
 
-// Waves of one prefix-kernel instantiation that fit on the device at once
-// (occupancy per CU x CU count), looked up once per instantiation.
-template <int D, int RB, int TILES>
+// Waves of one prefix-kernel instantiation (ROWS: the one with logit rows in
+// front) that fit on the device at once (occupancy per CU x CU count), looked
+// up once per instantiation.
+template <int D, int RB, int TILES, bool ROWS>
 int prefix_slots() {
   static std::atomic<int> cached{0};
   int v = cached.load(std::memory_order_relaxed);
@@ -1192,36 +1245,54 @@ int prefix_slots() {
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     cus = 256;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_prefix_bf16<D, RB, TILES, 2>, 64,
-                                                    prefix_lds_bytes<D>(RB)) != hipSuccess ||
-      per_cu <= 0)
-    per_cu = 4;
+  hipError_t e;
+  if constexpr (ROWS)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_prefix_rows_bf16<D, RB, TILES, 2>, 64,
+                                                     prefix_lds_bytes<D>(RB));
+  else
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_prefix_bf16<D, RB, TILES, 2>, 64,
+                                                     prefix_lds_bytes<D>(RB));
+  if (e != hipSuccess || per_cu <= 0) per_cu = 4;
   v = cus * per_cu;
   cached.store(v, std::memory_order_relaxed);
   return v;
 }
 
-template <int D>
+template <int D, bool ROWS>
 int prefix_slots_for(int rb) {
   switch (rb) {
-    case 1: return prefix_slots<D, 1, 2>();
-    case 2: return prefix_slots<D, 2, 2>();
-    case 3: return prefix_slots<D, 3, 1>();
-    default: return prefix_slots<D, 4, 1>();
+    case 1: return prefix_slots<D, 1, 2, ROWS>();
+    case 2: return prefix_slots<D, 2, 2, ROWS>();
+    case 3: return prefix_slots<D, 3, 1, ROWS>();
+    default: return prefix_slots<D, 4, 1, ROWS>();
   }
+}
+
+long slots_for(int D, int rb, bool rows) {
+  if (D == 128) return rows ? prefix_slots_for<128, true>(rb) : prefix_slots_for<128, false>(rb);
+  return rows ? prefix_slots_for<64, true>(rb) : prefix_slots_for<64, false>(rb);
 }
 
 }  // namespace
 
-void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int *nsplit, int *span,
+void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int ent_rows, int *nsplit, int *span,
                         int *nwaves) {
   // One round of waves: as many as fit on the chip at once, each taking an
   // equal span (whole 32-key chunks, at least 512 keys) of the flattened
   // (prefix, layer, KV head, key) space. A unit of plen keys is then covered
-  // by at most ceil(plen / span) + 1 spans.
+  // by at most ceil(plen / span) + 1 spans. Logit-row waves in the same
+  // launch take their slots first (the context waves keep at least half), and
+  // the context waves never outnumber those of the plan without rows, so that
+  // plan's workspace size covers both.
   const int rb = (rows + 15) / 16;
   const long total = (long)P * L * Hkv * plen;
-  const long slots = D == 128 ? prefix_slots_for<128>(rb) : prefix_slots_for<64>(rb);
+  long slots = slots_for(D, rb, false);
+  if (ent_rows > 0) {
+    const long with_rows = slots_for(D, rb, true);
+    const long all = with_rows < slots ? with_rows : slots;
+    slots = all - ent_rows > all / 2 ? all - ent_rows : all / 2;
+    if (slots < 1) slots = 1;
+  }
   long sp = (total + slots - 1) / slots;
   sp = (sp + 31) / 32 * 32;
   if (sp < 512) sp = 512;
@@ -1254,7 +1325,6 @@ hipError_t launch_decode_attn(const AttnParams &p, const EntropyBatch *ent, hipS
     }
     return hipGetLastError();
   }
-  if (ent && p.P > 0) return hipErrorInvalidValue;
   return p.D == 128 ? launch_bf16<128>(p, ent, stream) : launch_bf16<64>(p, ent, stream);
 }
 

@@ -38,15 +38,18 @@ struct AttnParams {
   int merge_pf, merge_blk;
 };
 
-// Work plan of the prefix path (rows = C * G query rows per prefix unit);
-// identical on the size query and the call.
-void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int *nsplit, int *span,
+// Work plan of the prefix path (rows = C * G query rows per prefix unit;
+// ent_rows = logit rows computed in the context launch, 0 for none);
+// identical on the size query and the call. The plan with ent_rows > 0 never
+// has more splits than the one without.
+void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int ent_rows, int *nsplit, int *span,
                         int *nwaves);
 size_t attn_workspace_bytes(int S, int L, int Hq, int D, int nsplit);
 
 struct EntropyBatch;
-// ent: NULL, or the entropy rows computed in the same launch (own cache
-// only, no prefix; rows 16-byte aligned, no workspace).
+// ent: NULL, or the entropy rows computed in the same launch (rows 16-byte
+// aligned, no workspace): with the own-cache kernel, or with a prefix in the
+// context kernel (p planned with ent_rows = the batch's rows).
 hipError_t launch_decode_attn(const AttnParams &p, const EntropyBatch *ent, hipStream_t stream);
 
 struct ScoreParams {

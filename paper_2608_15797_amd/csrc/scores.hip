@@ -354,6 +354,10 @@ __global__ __launch_bounds__(NW * 64) void window_scores_tiled(ScoreParams p) {
       const uint32_t off = ((uint32_t)(kt * kTK + row) * RU + (uint32_t)u) * 16u;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void_t *)(slot + I * 1024), 16, off, 0, 0, 0);
     }
+#else
+    (void)kt;  // the host pass has no buffer-to-LDS loads
+    (void)kr;
+    (void)RPI;
 #endif
   };
   // Wait for this wave's loads of the current tile, with `next` of its loads

@@ -96,11 +96,12 @@ def _load():
     lib.kvr_logit_entropy_batch.restype = ctypes.c_int
     lib.kvr_logit_entropy_batch_workspace_size.argtypes = [P(c_logit_set), i32]
     lib.kvr_logit_entropy_batch_workspace_size.restype = sz
-    lib.kvr_decode_attn_entropy.argtypes = [P(c_cache), vp, vp, i32, f32, vp, vp, vp, vp, P(c_policy), vp,
-                                            P(c_logit_set), i32, vp]
+    lib.kvr_decode_attn_entropy.argtypes = [P(c_cache), P(c_prefix), vp, vp, i32, f32, vp, vp, vp, vp,
+                                            P(c_policy), vp, vp, sz, P(c_logit_set), i32, vp]
     lib.kvr_decode_attn_entropy.restype = ctypes.c_int
-    lib.kvr_decode_attn_entropy_sample.argtypes = [P(c_cache), vp, vp, i32, f32, vp, vp, vp, vp, P(c_policy), vp,
-                                                   P(c_logit_set), i32, P(c_sampler), P(vp), vp]
+    lib.kvr_decode_attn_entropy_sample.argtypes = [P(c_cache), P(c_prefix), vp, vp, i32, f32, vp, vp, vp, vp,
+                                                   P(c_policy), vp, vp, sz, P(c_logit_set), i32, P(c_sampler),
+                                                   P(vp), vp]
     lib.kvr_decode_attn_entropy_sample.restype = ctypes.c_int
     lib.kvr_logit_entropy_batch_noalloc.argtypes = [P(c_logit_set), i32, vp]
     lib.kvr_logit_entropy_batch_noalloc.restype = ctypes.c_int
@@ -245,39 +246,46 @@ def decode_attn(cache: Cache, len_: torch.Tensor, q: torch.Tensor, out: torch.Te
 
 
 def decode_attn_entropy(cache: Cache, len_: torch.Tensor, q: torch.Tensor, out: torch.Tensor, scale: float,
-                        sets, k_new=None, v_new=None, new_pos=None, policy: Optional[Policy] = None,
-                        scores: Optional[torch.Tensor] = None, stream=None) -> None:
-    """kvr_decode_attn_entropy: decode_attn over the own caches plus the
-    entropies of the LogitSet list `sets` in the same launch."""
+                        sets, k_new=None, v_new=None, new_pos=None, prefix: Optional[Prefix] = None,
+                        policy: Optional[Policy] = None, scores: Optional[torch.Tensor] = None,
+                        workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """kvr_decode_attn_entropy: decode_attn plus the entropies of the LogitSet
+    list `sets` in the same launch (the context launch with a prefix)."""
     cc = cache.c()
+    pc = prefix.c() if prefix is not None else None
     pol = policy.c() if policy is not None else None
-    for t in (len_, q, out, k_new, v_new, new_pos, scores):
+    for t in (len_, q, out, k_new, v_new, new_pos, scores, workspace):
         assert t is None or t.is_contiguous()
     arr = _logit_sets(sets)
-    rc = lib.kvr_decode_attn_entropy(ctypes.byref(cc), _ptr(len_), _ptr(q), q.shape[2], float(scale),
-                                     _ptr(k_new), _ptr(v_new), _ptr(new_pos), _ptr(out),
-                                     ctypes.byref(pol) if pol else None, _ptr(scores), arr, len(sets),
-                                     _stream(stream))
+    rc = lib.kvr_decode_attn_entropy(ctypes.byref(cc), ctypes.byref(pc) if pc else None, _ptr(len_), _ptr(q),
+                                     q.shape[2], float(scale), _ptr(k_new), _ptr(v_new), _ptr(new_pos), _ptr(out),
+                                     ctypes.byref(pol) if pol else None, _ptr(scores), _ptr(workspace),
+                                     0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                     arr, len(sets), _stream(stream))
     _check(rc, "kvr_decode_attn_entropy")
 
 
 def decode_attn_entropy_sample(cache: Cache, len_: torch.Tensor, q: torch.Tensor, out: torch.Tensor, scale: float,
                                sets, sampler, tokens, k_new=None, v_new=None, new_pos=None,
-                               policy: Optional[Policy] = None, scores: Optional[torch.Tensor] = None,
+                               prefix: Optional[Prefix] = None, policy: Optional[Policy] = None,
+                               scores: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                                stream=None) -> None:
     """kvr_decode_attn_entropy_sample: decode_attn_entropy plus the next token
     of every row of every LogitSet; `tokens` holds one int32 tensor per set."""
     cc = cache.c()
+    pc = prefix.c() if prefix is not None else None
     pol = policy.c() if policy is not None else None
-    for t in (len_, q, out, k_new, v_new, new_pos, scores, *tokens):
+    for t in (len_, q, out, k_new, v_new, new_pos, scores, workspace, *tokens):
         assert t is None or t.is_contiguous()
     assert len(tokens) == len(sets)
     arr = _logit_sets(sets)
     tp = (ctypes.c_void_p * len(tokens))(*[t.data_ptr() for t in tokens])
-    rc = lib.kvr_decode_attn_entropy_sample(ctypes.byref(cc), _ptr(len_), _ptr(q), q.shape[2], float(scale),
-                                            _ptr(k_new), _ptr(v_new), _ptr(new_pos), _ptr(out),
-                                            ctypes.byref(pol) if pol else None, _ptr(scores), arr, len(sets),
-                                            ctypes.byref(sampler.c()), tp, _stream(stream))
+    rc = lib.kvr_decode_attn_entropy_sample(ctypes.byref(cc), ctypes.byref(pc) if pc else None, _ptr(len_),
+                                            _ptr(q), q.shape[2], float(scale), _ptr(k_new), _ptr(v_new),
+                                            _ptr(new_pos), _ptr(out), ctypes.byref(pol) if pol else None,
+                                            _ptr(scores), _ptr(workspace),
+                                            0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                            arr, len(sets), ctypes.byref(sampler.c()), tp, _stream(stream))
     _check(rc, "kvr_decode_attn_entropy_sample")
 
 

@@ -11,7 +11,8 @@ helper candidates of every problem decode together) is:
              moving-average detector on the base rows (Eq. (4); only base
              candidates are screened): computed in the base-attention launch
              of step 1 (kvr_decode_attn_entropy) when the workload has a base
-             model, else by one kvr_logit_entropy_batch call.
+             model, else in the helper's context launch of step 3 (the same
+             call with the prefix).
 
 All candidates advance in lockstep, so every live length is known on the host
 in advance: the driver precomputes per-token length tables on the device
@@ -107,8 +108,9 @@ class Decoder:
             wsb = kvr.decode_attn_workspace_size(self.hcache, self.prefix if with_helper_prefix else None,
                                                  h.Hq)
             self.hws = torch.empty(max(wsb, 16) // 4 + 4, dtype=torch.float32, device=dev)
-        # Entropies ride in the base-attention launch when there is one.
-        self.fuse_entropy = bool(b and wl.logits)
+        # Entropies ride in the base-attention launch when there is one, else
+        # in the helper's context launch.
+        self.fuse_entropy = bool(wl.logits)
         self.H = []
         self.ews = []
         for ls in wl.logits:
@@ -207,8 +209,16 @@ class Decoder:
                                 k_new=si.bk, v_new=si.bv, new_pos=self.bpos[t], policy=self.policy,
                                 scores=self.scores, stream=stream)
 
-    def helper_token(self, step: int, si: StepInputs, stream=None, timers=None, only=None) -> None:
+    def helper_token(self, step: int, si: StepInputs, stream=None, timers=None, only=None, sets=None) -> None:
+        """Helper attention of decode step `step`, with the entropies of
+        `sets` (LogitSet list) in the context launch when given."""
         h = self.wl.helper
+        if sets:
+            with _timer(timers, "helper_attn_entropy", stream, only):
+                kvr.decode_attn_entropy(self.hcache, self.hlen[step], si.hq, self.hout, h.softmax_scale, sets,
+                                        k_new=si.hk, v_new=si.hv, prefix=self.prefix, workspace=self.hws,
+                                        stream=stream)
+            return
         with _timer(timers, "helper_attn", stream, only):
             kvr.decode_attn(self.hcache, self.hlen[step], si.hq, self.hout, h.softmax_scale,
                             k_new=si.hk, v_new=si.hv, prefix=self.prefix, workspace=self.hws,
@@ -244,7 +254,8 @@ class Decoder:
             self.base_token(t, si, stream, timers=timers, evict_log=evict_log, only=only,
                             sets=self.logit_sets(si) if fused else None)
         if self.wl.helper:
-            self.helper_token(step, si, stream, timers=timers, only=only)
+            self.helper_token(step, si, stream, timers=timers, only=only,
+                              sets=self.logit_sets(si) if fused and not self.wl.base else None)
         if not fused:
             self.entropy(si, stream, timers=timers, only=only)
 

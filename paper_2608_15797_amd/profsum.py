@@ -40,8 +40,9 @@ CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 # Sources whose kernels each call runs (a record stays valid while they do not change).
 CALL_SOURCES = {
     "base_attn": ("attn.hip", "kvr_device.h"),
-    "base_attn_entropy": ("attn.hip", "entropy_common.h", "kvr_device.h"),
+    "base_attn_entropy": ("attn.hip", "entropy_common.h", "sampler_common.h", "kvr_device.h"),
     "helper_attn": ("attn.hip", "kvr_device.h"),
+    "helper_attn_entropy": ("attn.hip", "entropy_common.h", "sampler_common.h", "kvr_device.h"),
     "evict": ("evict.hip", "kvr_device.h"),
     "entropy": ("entropy.hip", "entropy_common.h", "kvr_device.h"),
 }
@@ -55,6 +56,8 @@ CALL_KERNELS = {
     "base_attn": (r"attn_cache_bf16<\d+, false, \d+, \d+, (true|false), 0>",),
     "base_attn_entropy": (r"attn_cache_bf16<\d+, false, \d+, \d+, (true|false), [12]>",),
     "helper_attn": (r"attn_prefix_bf16<", r"attn_cache_bf16<\d+, true"),
+    # The context kernel with the logit rows in front, then the suffix kernel.
+    "helper_attn_entropy": (r"attn_prefix_rows_bf16<", r"attn_cache_bf16<\d+, true"),
     "evict": (r"evict_topb_kernel",),
     "entropy": (r"entropy_kernel<", r"?entropy_merge"),
 }

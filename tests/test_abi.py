@@ -229,14 +229,36 @@ def test_decode_attn_entropy_rejects_on_host():
     c = _cache(kvr)
     arr = (kvr.c_logit_set * 1)()
     arr[0] = kvr.c_logit_set(16, 1, 4, 1001, 1001, 1.0, 16, None)  # ld * 2 = 2002 bytes
-    assert f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1, None) == -1
+    assert f(ctypes.byref(c), None, 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 0, arr, 1, None) == -1
     assert "aligned" in kvr.lib.kvr_last_error().decode()
     arr[0] = kvr.c_logit_set(16, 1, 4, 10, 5, 1.0, 16, None)  # ld < V
-    assert f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1, None) == -1
+    assert f(ctypes.byref(c), None, 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 0, arr, 1, None) == -1
     bad = _cache(kvr, D=96)
     arr[0] = kvr.c_logit_set(16, 1, 4, 1024, 1024, 1.0, 16, None)
-    assert f(ctypes.byref(bad), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1, None) == -2
-    assert f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 1, None) == -1
+    assert f(ctypes.byref(bad), None, 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 0, arr, 1, None) == -2
+    assert f(ctypes.byref(c), None, 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 0, None, 1, None) == -1
+
+
+def test_decode_attn_entropy_with_prefix_rejects_on_host():
+    """With a prefix the fused call needs kvr_decode_attn's workspace, and
+    scoring stays unavailable, as for kvr_decode_attn."""
+    from paper_2608_15797_amd import kvr
+    f = kvr.lib.kvr_decode_attn_entropy
+    c = _cache(kvr, S=16, Hkv=2, cap=512)
+    p = kvr.c_prefix(16, 16, 2, 8192)
+    arr = (kvr.c_logit_set * 1)()
+    arr[0] = kvr.c_logit_set(16, 1, 8, 151936, 151936, 1.0, 16, None)
+    need = kvr.lib.kvr_decode_attn_workspace_size(ctypes.byref(c), ctypes.byref(p), 12)
+    assert need > 0
+
+    def call(ws, nbytes, pol=None, scores=None):
+        return f(ctypes.byref(c), ctypes.byref(p), 16, 16, 12, 1.0, None, None, None, 16,
+                 ctypes.byref(pol) if pol is not None else None, scores, ws, nbytes, arr, 1, None)
+
+    assert call(None, 0) == -4
+    assert call(16, need - 16) == -4 and "workspace" in kvr.lib.kvr_last_error().decode()
+    assert call(16, need, kvr.c_policy(64, 32, 64), 16) == -1
+    assert "prefix" in kvr.lib.kvr_last_error().decode()
 
 
 def test_decode_attn_entropy_sample_rejects_on_host():
@@ -251,7 +273,7 @@ def test_decode_attn_entropy_sample_rejects_on_host():
     none = (ctypes.c_void_p * 1)(None)
 
     def call(smp, t=toks):
-        return f(ctypes.byref(c), 16, 16, 8, 1.0, None, None, None, 16, None, None, arr, 1,
+        return f(ctypes.byref(c), None, 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 0, arr, 1,
                  ctypes.byref(smp) if smp is not None else None, t, None)
 
     assert call(None) == -1 and "sampler" in kvr.lib.kvr_last_error().decode()

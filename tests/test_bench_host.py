@@ -37,22 +37,27 @@ def test_step_bytes_calls(name, fused):
     from paper_2608_15797_amd import benchplan as bench
     wl = WORKLOADS[name]
     dec = _decoder_stub(wl)
-    dec.fuse_entropy = fused and wl.base is not None
+    dec.fuse_entropy = fused
     e = 2  # bf16 logits
     logit_bytes = sum(ls.R * ls.V * e + ls.R * 4 for ls in wl.logits)
     evict_steps = 0
     for i in range(wl.steps):
         out = bench.step_bytes(wl, dec, i)
-        if dec.fuse_entropy:
+        if fused and wl.base:
             # The entropies ride in the base-attention launch: that call carries the logit bytes.
             n = dec.blen_host[dec.T_prompt + i]
             assert "entropy" not in out and "base_attn" not in out
             assert out["base_attn_entropy"] == bench.acc.base_attn_bytes(wl, n) + logit_bytes
+            assert ("helper_attn" in out) == (wl.helper is not None)
+        elif fused:
+            # Helper only: they ride in the helper's context launch.
+            assert "entropy" not in out and "helper_attn" not in out
+            assert out["helper_attn_entropy"] == bench.acc.helper_attn_bytes(wl, dec.hlen_host[i]) + logit_bytes
         else:
             # One batched entropy call per step covers every logit set.
             assert out["entropy"] == logit_bytes
             assert ("base_attn" in out) == (wl.base is not None)
-        assert ("helper_attn" in out) == (wl.helper is not None)
+            assert ("helper_attn" in out) == (wl.helper is not None)
         if wl.base:
             n = dec.blen_host[dec.T_prompt + i]
             assert ("evict" in out) == (n > wl.base.B + wl.base.buffer)

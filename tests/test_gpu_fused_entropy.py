@@ -10,6 +10,11 @@ every entropy must be within 1e-4 of the oracle, and the detector state
 Cases cover both cache types, bf16 and float32 logits, several sets with
 their own vocabulary, stride and temperature, a vocabulary below one 8-logit
 vector and one that is not a multiple of 8, -inf entries and a boosted row.
+
+With a prefix (the helper path) the rows ride in the context launch, whose
+split plan leaves their waves slots of their own: the outputs there are
+compared with the oracle at the helper path's tolerance, the appended rows
+bit for bit with kvr_decode_attn's.
 """
 import math
 
@@ -18,7 +23,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import as_f64, host, say
+from gpu_util import as_f64, host, rowwise_rel_err, say
 
 pytestmark = pytest.mark.gpu
 
@@ -206,3 +211,105 @@ def test_decode_attn_entropy_sample_matches_separate_calls(ci):
         d = np.abs(sets[j].H.cpu().double().numpy() - href).max()
         say("  set", j, "tokens", got[:8].tolist(), "oracle-exact", exact, "near-threshold", loose, "H err", d)
         assert d <= 1e-4
+
+
+PREFIX_CASES = [
+    # helper (S, P, L, Hkv, G, D, plen, scap, dtype), logit dtype, sets [(R, V, ld, kind, detector)], sampler
+    # Private 4096-token contexts of the helper-only workload's shape, 8 rows of its vocabulary.
+    ((8, 8, 2, 2, 6, 128, 4096, 40, torch.bfloat16), torch.bfloat16, [(8, 151936, 151936, "boosted", True)], None),
+    # 8 candidates x 6 heads share each context (three row blocks); float32 logits, two sets.
+    ((16, 2, 2, 2, 6, 128, 777, 40, torch.bfloat16), torch.float32,
+     [(5, 1023, 1024, "2.0", True), (3, 5, 8, "1.0", False)], None),
+    # Head dim 64, spans crossing units; the sampler draws every row's token.
+    ((6, 3, 2, 2, 6, 64, 513, 20, torch.bfloat16), torch.bfloat16,
+     [(6, 4099, 4104, "boosted", False), (2, 151936, 151936, "ties", False)], (0.8, 20, 0.95, 77, 3)),
+    # More rows than half the chip's context waves (1024 at one row block): the
+    # plan keeps 512 for the 524288 context keys (spans of 1024 keys, not 512).
+    ((4, 4, 4, 2, 6, 128, 16384, 16, torch.bfloat16), torch.bfloat16, [(1500, 64, 64, "2.0", False)], None),
+    # float32 caches: the entropy rows run as a kernel of their own after the attention kernel.
+    ((4, 2, 2, 2, 6, 128, 200, 24, torch.float32), torch.float32, [(4, 1024, 1024, "2.0", True)], None),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(PREFIX_CASES)))
+def test_decode_attn_entropy_with_prefix(ci):
+    """kvr_decode_attn_entropy(_sample) with a prefix: the logit rows ride in
+    the context launch. Attention outputs within the helper path's tolerance
+    of the oracle (the split points differ from kvr_decode_attn's, so the
+    outputs agree with it to rounding, not bit for bit), the appended suffix
+    rows bit for bit, entropies within 1e-4 of the oracle, the detector as
+    the oracle's, and the tokens those of kvr_logit_entropy_sample."""
+    from paper_2608_15797_amd import kvr as k
+    from test_gpu_sampler import _check_tokens, _logits
+    (S, P, L, Hkv, G, D, plen, scap, dt), ldt, specs, smp_args = PREFIX_CASES[ci]
+    say("case", ci, "helper", PREFIX_CASES[ci][0], "logits", ldt, "sets", specs, "sampler", smp_args)
+    Hq = Hkv * G
+    g = torch.Generator().manual_seed(6161 + ci)
+    scale = 1.0 / math.sqrt(D)
+    PK = _randn((P, L, Hkv, plen, D), g, dt)
+    PV = _randn((P, L, Hkv, plen, D), g, dt)
+    K = _randn((S, L, Hkv, scap, D), g, dt)
+    V = _randn((S, L, Hkv, scap, D), g, dt)
+    lens = torch.randint(1, scap + 1, (S,), generator=g, dtype=torch.int32)
+    lens[0] = 1
+    lens[-1] = scap
+    q = _randn((S, L, Hq, D), g, dt)
+    kn = _randn((S, L, Hkv, D), g, dt)
+    vn = _randn((S, L, Hkv, D), g, dt)
+    prefix = k.Prefix(PK.to(DEV), PV.to(DEV))
+    ca, cb = (k.Cache(K.to(DEV), V.to(DEV), None) for _ in range(2))
+    nws = k.decode_attn_workspace_size(ca, prefix, Hq)
+    wsa = torch.full((max(nws, 16) // 4,), float("nan"), device=DEV)
+    wsb = torch.full((max(nws, 16) // 4,), float("nan"), device=DEV)
+    oa = torch.empty((S, L, Hq, D), dtype=dt, device=DEV)
+    ob = torch.empty_like(oa)
+    lent = lens.to(DEV)
+    k.decode_attn(ca, lent, q.to(DEV), oa, scale, k_new=kn.to(DEV), v_new=vn.to(DEV), prefix=prefix, workspace=wsa)
+    xs = [_logits(R, V_, ld, ldt, kind, 91 + j) for j, (R, V_, ld, kind, det) in enumerate(specs)]
+    sets = [k.LogitSet(x.to(DEV), torch.full((x.shape[0],), float("nan"), device=DEV), V_, 1.0,
+                       k.Detector.zeros(x.shape[0], window=12, guard=0, tau=5.0, device=DEV) if det else None)
+            for x, (R, V_, ld, kind, det) in zip(xs, specs)]
+    smp = k.Sampler(*smp_args) if smp_args else None
+    if smp is None:
+        k.decode_attn_entropy(cb, lent, q.to(DEV), ob, scale, sets, k_new=kn.to(DEV), v_new=vn.to(DEV),
+                              prefix=prefix, workspace=wsb)
+    else:
+        toks = [torch.full((x.shape[0],), -7, dtype=torch.int32, device=DEV) for x in xs]
+        k.decode_attn_entropy_sample(cb, lent, q.to(DEV), ob, scale, sets, smp, toks, k_new=kn.to(DEV),
+                                     v_new=vn.to(DEV), prefix=prefix, workspace=wsb)
+    torch.cuda.synchronize()
+    Kh, Vh = K.clone(), V.clone()
+    for s in range(S):
+        n = int(lens[s])
+        Kh[s, :, :, n - 1] = kn[s]
+        Vh[s, :, :, n - 1] = vn[s]
+    ref, _ = oracle.decode_attn(host(Kh), host(Vh), lens.numpy(), host(q), scale,
+                                prefix_K=host(PK), prefix_V=host(PV), want_psum=False)
+    tol = 2e-2 if dt == torch.bfloat16 else 1e-5
+    ea, eb = rowwise_rel_err(as_f64(oa), ref).max(), rowwise_rel_err(as_f64(ob), ref).max()
+    say("  attention rel err: kvr_decode_attn %.2e, fused %.2e" % (ea, eb))
+    assert eb <= tol
+    bits = (lambda t: t.cpu().view(torch.int16)) if dt == torch.bfloat16 else (lambda t: t.cpu())
+    for t in ("k", "v"):
+        assert torch.equal(bits(getattr(ca, t)), bits(getattr(cb, t)))
+    for j, (x, (R, V_, ld, kind, det)) in enumerate(zip(xs, specs)):
+        href = oracle.entropy(host(x), V=V_)
+        d = np.abs(sets[j].H.cpu().double().numpy() - href).max()
+        say("  set", j, "rows", R, "H err", d)
+        assert d <= 1e-4
+        if det:
+            od = oracle.Detector(R, window=12, guard=0, tau=5.0)
+            fref = od.step(href)
+            assert sets[j].detector.cnt.cpu().numpy().tolist() == [1] * R
+            f = sets[j].detector.flag.cpu().numpy()
+            assert ((f == fref) | (np.abs(href - 5.0) < 1e-4)).all()
+        if smp is not None:
+            got = toks[j].cpu().numpy()
+            H = torch.empty(R, device=DEV)
+            ref_tok = torch.full((R,), -7, dtype=torch.int32, device=DEV)
+            ws = torch.empty(max(k.logit_entropy_sample_workspace_size(R, V_, smp.top_k), 16) // 4 + 4, device=DEV)
+            k.logit_entropy_sample(x.to(DEV), H, ref_tok, smp, V=V_, workspace=ws)
+            torch.cuda.synchronize()
+            assert (got == ref_tok.cpu().numpy()).all(), (j, got, ref_tok.cpu().numpy())
+            exact, loose = _check_tokens(host(x), V_, smp, got)
+            say("  set", j, "tokens oracle-exact", exact, "near-threshold", loose)

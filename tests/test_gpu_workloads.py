@@ -167,7 +167,9 @@ def test_workload_lockstep(name):
             hs = sorted(x for g in groups.values() for x in g)
             Kh_pre = host(dec.hcache.k[hs])
             Vh_pre = host(dec.hcache.v[hs])
-            dec.helper_token(i, si)
+            # The product path: with no base model the entropies ride in the
+            # helper's context launch.
+            dec.helper_token(i, si, sets=dec.logit_sets(si) if (dec.fuse_entropy and not b) else None)
             torch.cuda.synchronize()
             K, V = Kh_pre.copy(), Vh_pre.copy()
             K[:, :, :, u - 1] = host(si.hk[hs])
@@ -186,7 +188,7 @@ def test_workload_lockstep(name):
                 % (len(hs), "all" if every else "one per problem", h.plen, u, worst))
             if every:
                 assert len(hs) == h.S
-        if not (b and dec.fuse_entropy):
+        if not dec.fuse_entropy:
             dec.entropy(si)
         torch.cuda.synchronize()
         for w, ls in enumerate(wl.logits):
