@@ -25,6 +25,15 @@
 //                all of a head's reads in flight before its writes);
 //       copy     a contiguous copy of the same number of bytes per head;
 //       flat     one flat streaming copy of the same total bytes, grid-stride.
+//   streamprobe read MB [MB ...]
+//     Read-only streams of MB megabytes (10^6 bytes), the bound of a call that
+//     only reads (the helper's context kernel reads 15032 MB per call of the
+//     72B + helper workload). Patterns:
+//       flat  grid-stride 16-byte loads, U per thread in flight, 256-thread
+//             workgroups, several grid sizes;
+//       span  the context kernel's split: one 64-lane wave per equal
+//             contiguous span, 1 KiB per load instruction, U in flight, for
+//             several wave counts (1024 = one wave per SIMD, as the kernel).
 //
 // Bytes are algorithmic: attention N rows x 512 bytes per unit; eviction the
 // moved rows x 512 bytes, read and written.
@@ -221,6 +230,45 @@ __global__ __launch_bounds__(256) void flat_copy(const u32x4 *src, u32x4 *dst, s
     __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
+// ------------------------------------------------------------ read-only streams
+
+template <int U>
+__global__ __launch_bounds__(256) void flat_read(const u32x4 *src, size_t n16, uint32_t *out) {
+  const size_t stride = (size_t)gridDim.x * 256;
+  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  uint32_t a = 0;
+  for (; i + (size_t)(U - 1) * stride < n16; i += (size_t)U * stride) {
+    u32x4 r[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) r[u] = __builtin_nontemporal_load(src + i + (size_t)u * stride);
+    a ^= fold(r, U);
+  }
+  for (; i < n16; i += stride) {
+    const u32x4 r = __builtin_nontemporal_load(src + i);
+    a ^= r.x ^ r.w;
+  }
+  out[(size_t)blockIdx.x * 256 + threadIdx.x] = a;
+}
+
+template <int U>
+__global__ __launch_bounds__(64) void span_read(const u32x4 *src, size_t n16, size_t span16, uint32_t *out) {
+  const size_t s0 = (size_t)blockIdx.x * span16;
+  const size_t s1 = s0 + span16 < n16 ? s0 + span16 : n16;
+  size_t i = s0 + threadIdx.x;
+  uint32_t a = 0;
+  for (; i + (size_t)(U - 1) * 64 < s1; i += (size_t)U * 64) {
+    u32x4 r[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) r[u] = __builtin_nontemporal_load(src + i + (size_t)u * 64);
+    a ^= fold(r, U);
+  }
+  for (; i < s1; i += 64) {
+    const u32x4 r = __builtin_nontemporal_load(src + i);
+    a ^= r.x ^ r.w;
+  }
+  out[(size_t)blockIdx.x * 64 + threadIdx.x] = a;
+}
+
 template <typename F>
 static double time_us(F f, int reps = 20) {
   hipEvent_t a, b;
@@ -328,6 +376,50 @@ static int run_evict(int heads, int cap, int B, int W, int n) {
   return 0;
 }
 
+static int run_read(const std::vector<double> &mbs) {
+  double mx = 0;
+  for (double m : mbs) {
+    if (!(m >= 1.0 && m <= 64000.0)) { printf("MB=%g outside 1..64000\n", m); return 1; }
+    mx = m > mx ? m : mx;
+  }
+  const size_t cap16 = (size_t)(mx * 1e6) / 16;
+  const int grids[4] = {1024, 2048, 4096, 8192};
+  const int waves[3] = {1024, 2048, 4096};
+  u32x4 *src;
+  uint32_t *out;
+  CK(hipMalloc(&src, cap16 * 16));
+  CK(hipMalloc(&out, (size_t)8192 * 256 * 4));  // the largest grid's threads
+  CK(hipMemset(src, 1, cap16 * 16));
+  for (double m : mbs) {
+    const size_t n16 = (size_t)(m * 1e6) / 16;
+    const double b = (double)n16 * 16;
+    for (int g : grids) {
+      for (int u : {8, 16}) {
+        double us = time_us([&] {
+          if (u == 8) hipLaunchKernelGGL(flat_read<8>, dim3(g), dim3(256), 0, 0, src, n16, out);
+          else hipLaunchKernelGGL(flat_read<16>, dim3(g), dim3(256), 0, 0, src, n16, out);
+        });
+        printf("read %.0f MB flat grid=%d U=%d %9.1f us %6.2f TB/s\n", m, g, u, us, b / (us * 1e-6) / 1e12);
+        fflush(stdout);
+      }
+    }
+    for (int w : waves) {
+      const size_t span16 = (n16 + w - 1) / w;
+      for (int u : {8, 16}) {
+        double us = time_us([&] {
+          if (u == 8) hipLaunchKernelGGL(span_read<8>, dim3(w), dim3(64), 0, 0, src, n16, span16, out);
+          else hipLaunchKernelGGL(span_read<16>, dim3(w), dim3(64), 0, 0, src, n16, span16, out);
+        });
+        printf("read %.0f MB span waves=%d U=%d %9.1f us %6.2f TB/s\n", m, w, u, us, b / (us * 1e-6) / 1e12);
+        fflush(stdout);
+      }
+    }
+  }
+  CK(hipFree(src));
+  CK(hipFree(out));
+  return 0;
+}
+
 int main(int argc, char **argv) {
   if (argc >= 5 && !strcmp(argv[1], "attn")) {
     std::vector<int> ns;
@@ -336,6 +428,11 @@ int main(int argc, char **argv) {
   }
   if (argc == 7 && !strcmp(argv[1], "evict"))
     return run_evict(atoi(argv[2]), atoi(argv[3]), atoi(argv[4]), atoi(argv[5]), atoi(argv[6]));
-  printf("usage: streamprobe attn UNITS CAP N [N ...] | streamprobe evict HEADS CAP B W N\n");
+  if (argc >= 3 && !strcmp(argv[1], "read")) {
+    std::vector<double> mbs;
+    for (int i = 2; i < argc; i++) mbs.push_back(atof(argv[i]));
+    return run_read(mbs);
+  }
+  printf("usage: streamprobe attn UNITS CAP N [N ...] | streamprobe evict HEADS CAP B W N | streamprobe read MB [MB ...]\n");
   return 2;
 }
