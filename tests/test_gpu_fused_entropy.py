@@ -226,6 +226,10 @@ PREFIX_CASES = [
     # More rows than half the chip's context waves (1024 at one row block): the
     # plan keeps 512 for the 524288 context keys (spans of 1024 keys, not 512).
     ((4, 4, 4, 2, 6, 128, 16384, 16, torch.bfloat16), torch.bfloat16, [(1500, 64, 64, "2.0", False)], None),
+    # 4 candidates x 8 heads (two row blocks) and 8 x 8 (four row blocks, the kernel that spills to scratch).
+    ((8, 2, 1, 2, 8, 128, 2100, 33, torch.bfloat16), torch.bfloat16, [(3, 151936, 151936, "boosted", True)], None),
+    ((8, 1, 1, 1, 8, 128, 300, 16, torch.bfloat16), torch.float32, [(4, 5000, 5000, "2.0", False)],
+     (0.8, 20, 0.95, 5, 1)),
     # float32 caches: the entropy rows run as a kernel of their own after the attention kernel.
     ((4, 2, 2, 2, 6, 128, 200, 24, torch.float32), torch.float32, [(4, 1024, 1024, "2.0", True)], None),
 ]
