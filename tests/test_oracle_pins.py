@@ -340,3 +340,15 @@ def test_detector_mean_is_over_last_window():
     flags = [int(det.step(np.array([h]))[0]) for h in seq]
     # means of the last 4: pos4 0, pos5 2.25 -> fires and stays set.
     assert flags == [0, 0, 0, 0, 1, 1, 1, 1, 1, 1, 1]
+
+
+def test_detector_mean_before_the_window_fills():
+    """With a guard shorter than the window, the moving mean runs over the
+    entropies pushed so far, not over a zero-padded window."""
+    det = oracle.Detector(2, window=12, guard=2, tau=7.0)
+    flags = [det.step(np.array([h, h - 6.0])).tolist() for h in (8.0, 8.0, 8.0)]
+    # Row 0: means 8, 8, 8 (fires from the guard on); over 12 slots they would
+    # be 0.67, 1.33, 2. Row 1: means 2, 2, 2, never.
+    assert flags == [[0, 0], [1, 0], [1, 0]]
+    assert det.cnt.tolist() == [3, 3]
+    np.testing.assert_array_equal(det.hist[0, :3], [8.0, 8.0, 8.0])

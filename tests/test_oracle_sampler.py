@@ -14,6 +14,9 @@
       generator's top 24 bits are uniform enough and the nucleus is right.
   Q6  temperature only rescales: the top-k set does not depend on it and a
       lower temperature concentrates the draw.
+  Q7  the inverse-CDF intervals are half-open: token i of the nucleus is
+      drawn for u * mass in [cum_{i-1}, cum_i), so u exactly at a cumulative
+      mass draws the next token.
 """
 import math
 
@@ -120,6 +123,19 @@ def test_q6_temperature():
     # temperature T equals logits divided by T at temperature 1
     _, d3 = sampler.sample_row(x / 0.25, 300, 1.0, 20, 1.0, 0.5)
     np.testing.assert_allclose(d2["q"], d3["q"], rtol=1e-12)
+
+
+def test_q7_draw_intervals_are_half_open():
+    # Four equal logits: probabilities exactly 1/4, cumulative masses 1/4, 1/2,
+    # 3/4, 1 (exact in binary, as are these 24-bit uniforms).
+    x = np.zeros(4)
+    for u, want in ((0.0, 0), (0.25 - 2.0 ** -24, 0), (0.25, 1), (0.5, 2), (0.75, 3), (1.0 - 2.0 ** -24, 3)):
+        tok, d = sampler.sample_row(x, 4, 1.0, 4, 1.0, u)
+        assert d["keep"] == 4 and tok == want, (u, tok)
+    # With a top-p cut the same holds on the kept prefix's mass (1/2 here).
+    for u, want in ((0.0, 0), (0.5, 1), (1.0 - 2.0 ** -24, 1)):
+        tok, d = sampler.sample_row(x, 4, 1.0, 4, 0.5, u)
+        assert d["keep"] == 2 and tok == want, (u, tok)
 
 
 def test_bf16_rows_are_widened_exactly():
