@@ -20,7 +20,8 @@ its observation window (the steps that stream the score), choosing among the
 workload's evictions the one whose window has the mean helper suffix length
 closest to the suffix cycle's mean. The W warmup
 steps are the W step indices just before the window; the step indices between
-the prompt and the warmup are not run. Without --steps, K is one whole cycle:
+the prompt and the warmup are not run. The defaults, K = 20 and W = 5, time
+one eviction with its observation window; --steps 0 times one whole cycle:
 whole eviction periods covering the 512-token helper suffix cycle.
 
 Inputs are synthetic and seeded, resident in HBM before timing starts. The
@@ -501,8 +502,8 @@ def rounded(d):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=0, help="timed steps (default: one whole cycle)")
-    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--steps", type=int, default=20, help="timed steps (0: one whole cycle)")
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--extra", default=",".join(DEFAULT_EXTRA),
                     help="comma-separated workloads also reported, each over one whole cycle (empty: none)")

@@ -47,7 +47,7 @@ def main(argv=None) -> None:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--workload", default="base72b_helper", choices=sorted(WORKLOADS))
     ap.add_argument("--steps", type=int, default=0, help="window steps (default: one whole cycle)")
-    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=5)
     args = ap.parse_args(argv)
     calibration_copy()
     print("calibration copy done", flush=True)
