@@ -240,8 +240,12 @@ EVICT_CASES = [
     (4, 3, 4, 128, 128, 32, 128, torch.bfloat16),
     (6, 2, 8, 128, 64, 32, 64, torch.bfloat16),
     (3, 2, 2, 128, 20, 5, 7, torch.float32),
-    # Largest cache the eviction kernel takes at B = 256: cap 8000, 63.5 KB of LDS.
+    # An 8000-slot cache (the commit path's one-shot compression): candidates past
+    # the select's registers, read back from LDS.
     (1, 1, 2, 128, 256, 32, 7743, torch.bfloat16),
+    # Largest cache the eviction kernel takes at B = 256: cap + B = 16384 slots,
+    # 64 KiB of LDS for the keys and the kept set.
+    (1, 1, 2, 128, 256, 32, 15871, torch.bfloat16),
 ]
 
 
