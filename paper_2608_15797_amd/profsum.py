@@ -129,7 +129,8 @@ def in_window(order, bounds) -> bool:
 
 
 def window_stats(db: str, window) -> list[str]:
-    """Per-kernel dispatch count and average duration within a marker window."""
+    """Per-kernel dispatch count and average duration within a marker window,
+    then the per-dispatch average of every collected PMC counter there."""
     rows = dispatch_rows(db)
     bounds = window_orders(rows, window)
     agg = collections.defaultdict(lambda: [0.0, 0])
@@ -137,8 +138,11 @@ def window_stats(db: str, window) -> list[str]:
         if keep(r["name"]) and in_window(r["order"], bounds):
             agg[r["name"]][0] += r["dur_ns"]
             agg[r["name"]][1] += 1
-    return ["duration  %-78s calls %7d  avg_us %10.2f" % (n[:78], k, t / k / 1e3)
-            for n, (t, k) in sorted(agg.items(), key=lambda x: -x[1][0])]
+    out = ["duration  %-78s calls %7d  avg_us %10.2f" % (n[:78], k, t / k / 1e3)
+           for n, (t, k) in sorted(agg.items(), key=lambda x: -x[1][0])]
+    for (name, cn), (v, n) in sorted(counters(db, window).items()):
+        out.append("counter   %-78s %-24s avg %16.1f  (dispatches %d)" % (name[:78], cn, v / n, n))
+    return out
 
 
 def _dbs(d: str) -> list[str]:
