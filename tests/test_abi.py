@@ -28,6 +28,44 @@ def test_library_exports_every_declared_symbol():
     assert set(declared_functions()) == set(kvr.EXPORTS)
 
 
+C_CALLER = r"""
+#include <stdio.h>
+#include <string.h>
+#include "kvr.h"
+int main(void) {
+  kvr_cache c;
+  memset(&c, 0, sizeof c);
+  int st = kvr_evict_topb(&c, NULL, NULL, NULL, NULL, NULL, NULL);
+  printf("%s|%d|%s\n", kvr_strerror(KVR_OK), st, kvr_last_error());
+  return st == KVR_EINVAL ? 0 : 1;
+}
+"""
+
+
+@pytest.mark.skipif(not os.path.exists("/opt/rocm/include/hip/hip_runtime_api.h"), reason="HIP headers absent")
+def test_header_is_a_c_abi(tmp_path):
+    """include/kvr.h compiles as C11 without warnings, and a C program links
+    against libkvr.so and gets a host-side rejection with its message."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    from paper_2608_15797_amd import kvr
+    src = tmp_path / "caller.c"
+    src.write_text(C_CALLER)
+    exe = str(tmp_path / "caller")
+    libdir = os.path.dirname(kvr.LIB_PATH)
+    r = subprocess.run(["gcc", "-std=c11", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                        "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include", str(src),
+                        "-L", libdir, "-lkvr", "-Wl,-rpath," + libdir, "-o", exe],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    out = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert out.returncode == 0, out.stdout + out.stderr
+    ok, status, msg = out.stdout.strip().split("|")
+    assert ok == "ok" and int(status) == -1 and "NULL" in msg
+
+
 def test_status_strings():
     from paper_2608_15797_amd import kvr
     assert kvr.lib.kvr_strerror(0) == b"ok"
