@@ -54,6 +54,13 @@ BASE_CASES = [
     (5, 1, 2, 4, 64, 12, 4, 6, torch.bfloat16),
     # Largest scored cache at G = 16: the window logits fill 61.6 KB of LDS (limit 64 KB).
     (2, 1, 1, 16, 128, 704, 64, 255, torch.bfloat16),
+    # Group sizes that fill the 16-row tile partially in other ways.
+    (3, 2, 2, 2, 128, 40, 8, 30, torch.bfloat16),
+    (3, 2, 2, 3, 128, 40, 8, 30, torch.bfloat16),
+    (2, 2, 2, 5, 64, 40, 8, 30, torch.bfloat16),
+    (2, 1, 2, 9, 128, 40, 8, 30, torch.bfloat16),
+    (2, 1, 2, 12, 128, 64, 32, 64, torch.bfloat16),
+    (2, 1, 1, 15, 128, 40, 8, 30, torch.bfloat16),
 ]
 
 
@@ -161,6 +168,10 @@ PREFIX_CASES = [
     (6, 3, 2, 2, 6, 64, 513, 20, torch.bfloat16),
     (8, 2, 2, 2, 6, 128, 150, 24, torch.bfloat16),    # spans of 512 keys cross up to 4 units
     (4, 2, 1, 2, 6, 128, 200, 24, torch.float32),
+    # Row counts that are not multiples of 16: 3 x 5 = 15, 5 x 7 = 35, 13 x 3 = 39.
+    (6, 2, 2, 2, 5, 128, 900, 20, torch.bfloat16),
+    (10, 2, 1, 2, 7, 128, 700, 20, torch.bfloat16),
+    (13, 1, 1, 2, 3, 64, 1100, 20, torch.bfloat16),
 ]
 
 
