@@ -143,3 +143,20 @@ WORKLOADS = {
                          near_uniform_frac=0.05),),
         seed=SEED_BASE + 5),
 }
+
+# The alternative readings reported beside the graded ones (same seeds and
+# inputs as the workload each varies): the helper-only contexts shared by all
+# 8 candidates, the 7B + helper contexts private to each candidate, the
+# 7B + helper base with a 128-slot buffer, and the 72B helper contexts shared
+# per problem (4 candidates each).
+WORKLOADS.update({
+    "helper4k_shared": WORKLOADS["helper4k"].with_(
+        name="helper4k_shared", helper=replace(WORKLOADS["helper4k"].helper, P=1)),
+    "base7b_helper_private": WORKLOADS["base7b_helper"].with_(
+        name="base7b_helper_private", helper=replace(WORKLOADS["base7b_helper"].helper, P=128)),
+    "base7b_helper_buf128": WORKLOADS["base7b_helper"].with_(
+        name="base7b_helper_buf128", base=replace(WORKLOADS["base7b_helper"].base, buffer=128)),
+    "base72b_helper_shared": WORKLOADS["base72b_helper"].with_(
+        name="base72b_helper_shared", helper=replace(WORKLOADS["base72b_helper"].helper, P=8)),
+})
+ALTERNATIVES = ("helper4k_shared", "base7b_helper_private", "base7b_helper_buf128", "base72b_helper_shared")
