@@ -426,10 +426,11 @@ size_t kvr_logit_entropy_sample_workspace_size(int32_t R, int32_t V, int32_t top
  *              of the two caches, copied alongside (streamed window sums that a
  *              fork inherits).
  * Consecutive destinations (groups of 8) that share a source are served by
- * one workgroup that reads the source once, so a source fanned out to N
- * consecutive candidates is read from HBM once per group.
+ * workgroups that read each piece of the source once, so a source fanned out
+ * to N consecutive candidates is read from HBM once per group.
  * Errors: KVR_EINVAL (shape or pointer mismatch, dst->pos without src->pos,
- * one of the score pointers NULL), KVR_EUNSUPPORTED (dtype, D), KVR_EHIP.
+ * one of the score pointers NULL), KVR_EUNSUPPORTED (dtype, D, L * Hkv above
+ * 32767 or dst->S above 524280), KVR_EHIP.
  */
 int kvr_fork(const kvr_cache *src, const kvr_cache *dst, const int32_t *src_index,
              const int32_t *len, const float *src_scores, float *dst_scores,

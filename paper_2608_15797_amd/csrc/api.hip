@@ -258,6 +258,9 @@ int kvr_fork(const kvr_cache *src, const kvr_cache *dst, const int32_t *src_inde
     return fail(KVR_EINVAL, "src and dst share k but are not the same cache");
   if (!same && (src->v == dst->v))
     return fail(KVR_EINVAL, "src and dst share v but not k");
+  if ((long)dst->L * dst->Hkv > kvr::kForkMaxLH || dst->S > kvr::kForkMaxDst)
+    return fail(KVR_EUNSUPPORTED, "fork of L*Hkv=%ld units over S=%d destinations (at most %ld and %ld)",
+                (long)dst->L * dst->Hkv, dst->S, kvr::kForkMaxLH, kvr::kForkMaxDst);
   kvr::ForkParams p{};
   p.sk = src->k; p.sv = src->v; p.spos = dst->pos ? src->pos : nullptr; p.ssc = src_scores;
   p.S_src = src->S; p.cap_src = src->cap;

@@ -144,6 +144,10 @@ struct ForkParams {
   int same;  // src and dst are the same cache
   const int32_t *src_index, *len;
 };
+// Largest L * Hkv and destination count one fork launch covers (its grid
+// holds L * Hkv * 2 and S_dst / 8 workgroups in two dimensions).
+constexpr long kForkMaxLH = 32767;
+constexpr long kForkMaxDst = 65535L * 8;
 hipError_t launch_fork(const ForkParams &p, hipStream_t stream);
 
 struct AppendParams {

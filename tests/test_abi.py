@@ -277,6 +277,23 @@ def test_decode_attn_entropy_rejects_on_host():
     assert f(ctypes.byref(c), None, 16, 16, 8, 1.0, None, None, None, 16, None, None, None, 0, None, 1, None) == -1
 
 
+def test_fork_rejects_shapes_beyond_its_grid_on_host():
+    """A fork launch covers at most 32767 (layer, KV head) units and 524280
+    destinations; larger shapes are refused before anything is enqueued."""
+    from paper_2608_15797_amd import kvr
+    f = kvr.lib.kvr_fork
+    for kw, msg in ((dict(L=16384, Hkv=2), "L*Hkv=32768"), (dict(S=524281), "S=524281")):
+        src = _cache(kvr, **{k: v for k, v in kw.items() if k != "S"})
+        dst = _cache(kvr, k=32, v=48, **kw)
+        assert f(ctypes.byref(src), ctypes.byref(dst), 16, 16, None, None, None) == -2
+        assert msg in kvr.lib.kvr_last_error().decode()
+    for kw in (dict(L=16383, Hkv=2), dict(S=524280, Hkv=1)):  # at the limits: on to the next check
+        src = _cache(kvr, **{k: v for k, v in kw.items() if k != "S"})
+        dst = _cache(kvr, k=32, v=48, **kw)
+        assert f(ctypes.byref(src), ctypes.byref(dst), None, 16, None, None, None) == -1
+        assert "src_index" in kvr.lib.kvr_last_error().decode()
+
+
 def test_decode_attn_entropy_with_prefix_rejects_on_host():
     """With a prefix the fused call needs kvr_decode_attn's workspace, and
     scoring stays unavailable, as for kvr_decode_attn."""
