@@ -145,6 +145,44 @@ def window_stats(db: str, window) -> list[str]:
     return out
 
 
+SUFFIX_KERNEL = re.compile(r"attn_cache_bf16<\d+, true")
+
+
+def suffix_fit(db: str, bench_json: str, window=(0, 1)) -> list[str]:
+    """Least-squares fit of the helper suffix kernel's duration against the
+    suffix length u of every step of a bench.py timed pass (the dispatches
+    between markers A and B of a kernel trace of that command): duration =
+    fixed + per_key * u. per_key against the bytes of one more suffix key
+    (K and V rows of every candidate's (layer, KV head) units) is the
+    kernel's streaming rate; fixed is what a call costs whatever u is."""
+    import numpy as np
+
+    from .benchplan import Schedule
+    from .workloads import WORKLOADS
+    with open(bench_json) as fh:
+        line = json.loads(fh.read().strip().splitlines()[-1])
+    wl = WORKLOADS[line["config"]["workload"]]
+    h = wl.helper
+    s0, K = line["config"]["window"]["first_step"], line["steps"]
+    rows = dispatch_rows(db)
+    bounds = window_orders(rows, window)
+    dur = np.array([r["dur_ns"] / 1e3 for r in rows
+                    if SUFFIX_KERNEL.search(r["name"]) and in_window(r["order"], bounds)])
+    if len(dur) != K:
+        raise SystemExit("%s: %d suffix dispatches in the window, %d timed steps" % (db, len(dur), K))
+    sch = Schedule(wl, s0 + K + 1)
+    u = np.array([sch.hlen_host[s0 + i] for i in range(K)], dtype=float)
+    fixed, per_key = np.linalg.lstsq(np.vstack([np.ones(K), u]).T, dur, rcond=None)[0]
+    resid = dur - (fixed + per_key * u)
+    key_bytes = h.S * h.L * h.Hkv * 2 * h.D * (4 if wl.dtype == "f32" else 2)
+    mean = dur.mean()
+    return ["suffix kernel, %s, %d timed steps (u = %d..%d, mean %.1f): duration = %.1f us + %.4f us x u "
+            "(rms residual %.1f us)" % (wl.name, K, u.min(), u.max(), u.mean(), fixed, per_key,
+                                        float(np.sqrt((resid ** 2).mean()))),
+            "  mean call %.1f us, fixed part %.1f%%; one more suffix key moves %d bytes: %.2f TB/s marginal"
+            % (mean, 100 * fixed / mean, key_bytes, key_bytes / (per_key * 1e-6) / 1e12)]
+
+
 def _dbs(d: str) -> list[str]:
     return sorted(glob.glob(d + "/**/*_results.db", recursive=True))
 
@@ -276,8 +314,18 @@ def main(argv=None):
     ap.add_argument("--alg", help="output of the profiled program: add its algorithmic bytes per dispatch")
     ap.add_argument("--window", nargs=2, type=int, metavar=("A", "B"),
                     help="only the dispatches between marker dispatches A and B")
+    ap.add_argument("--suffix-fit", metavar="BENCH_JSON",
+                    help="fit the helper suffix kernel's duration against the suffix length over the timed "
+                         "pass of this bench.py output (one trace directory; --window defaults to 0 1)")
     args = ap.parse_args(argv)
     window = tuple(args.window) if args.window else None
+    if args.suffix_fit:
+        if len(args.dirs) != 1:
+            raise SystemExit("--suffix-fit takes one kernel-trace result directory")
+        for db in _dbs(args.dirs[0]):
+            for line in suffix_fit(db, args.suffix_fit, window or (0, 1)):
+                print(line)
+        return
     if args.traffic:
         if len(args.dirs) != 2:
             raise SystemExit("--traffic takes the FETCH_SIZE and the WRITE_SIZE result directories")

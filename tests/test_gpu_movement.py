@@ -78,6 +78,34 @@ def test_fork_parity(dtype, D):
     _assert_state_equal(_np_state(src, ssc), ref_src)  # source untouched
 
 
+@pytest.mark.parametrize("dtype,D", [(torch.bfloat16, 128), (torch.float32, 64),
+                                     (torch.bfloat16, 64), (torch.float32, 128)])
+def test_fork_parity_across_pieces(dtype, D):
+    """Runs longer than a workgroup's piece of the slots (512 16-byte vectors:
+    16 to 64 slots by dtype and D), lengths on every side of the piece
+    boundaries, two destination groups of 8 (the second partial), a source
+    shared across the group boundary."""
+    g = torch.Generator().manual_seed(23 + D)
+    L, Hkv = 2, 3
+    piece = 512 * 16 // (D * torch.tensor([], dtype=dtype).element_size())
+    src = _cache(4, L, Hkv, 300, D, dtype, g)
+    dst = _cache(13, L, Hkv, 257, D, dtype, g)
+    ssc = torch.rand((4, L, Hkv, 300), generator=g).to(DEV)
+    dsc = torch.rand((13, L, Hkv, 257), generator=g).to(DEV)
+    idx = [0, 0, 1, 1, 1, 2, 3, 3, 3, 3, 0, 2, -1]
+    ln = [piece - 1, piece, piece + 1, 2 * piece + 3, 257, 300, 1, 0, 3 * piece, 4 * piece - 1,
+          5 * piece + 7, 100, 50]
+    ref_src = _np_state(src, ssc)
+    ref = _np_state(dst, dsc)
+    oln = [max(0, min(n, 257)) for n in ln]
+    movement.fork(ref_src, ref, idx, oln)
+    kvr().fork(src, dst, torch.tensor(idx, dtype=torch.int32, device=DEV),
+               torch.tensor(ln, dtype=torch.int32, device=DEV), ssc, dsc)
+    torch.cuda.synchronize()
+    _assert_state_equal(_np_state(dst, dsc), ref)
+    _assert_state_equal(_np_state(src, ssc), ref_src)
+
+
 def test_fork_without_pos_and_scores():
     g = torch.Generator().manual_seed(5)
     src = _cache(2, 2, 2, 24, 128, torch.bfloat16, g)

@@ -50,3 +50,43 @@ def test_default_roofline_from_stored_profile():
     h = rec["calls"]["helper_attn"]
     assert h["alg_bytes_per_dispatch"] == int(round(alg))
     assert 1.0 <= h["bytes_per_call"] / h["alg_bytes_per_dispatch"] < 1.01
+
+
+def test_suffix_fit_recovers_a_planted_line(tmp_path):
+    """profsum --suffix-fit on a synthetic kernel trace: suffix dispatches of
+    7 + 0.05 u microseconds (u from the workload's schedule), among other
+    dispatches and outside the marker window, give back 7 and 0.05."""
+    import sqlite3
+
+    from paper_2608_15797_amd import profsum
+    wl = WORKLOADS["helper4k"]
+    s0, K = 5, 40
+    sch = Schedule(wl, s0 + K + 1)
+    db = tmp_path / "run_results.db"
+    c = sqlite3.connect(db)
+    c.execute("create table kernels (dispatch_id integer, name text, start integer, end integer)")
+    rows, t, k = [], 0, 0
+
+    def put(name, us):
+        nonlocal t, k
+        rows.append((k, name, t, t + int(round(us * 1e3))))
+        t += int(round(us * 1e3)) + 100
+        k += 1
+
+    suffix = "void kvr::(anonymous namespace)::attn_cache_bf16<128, true, 2, 2, true, 0>(kvr::AttnParams)"
+    put(suffix, 999.0)  # before the window
+    put("at::native::spin_kernel(long)", 1.0)
+    for i in range(K):
+        put("void kvr::(anonymous namespace)::attn_prefix_rows_bf16<128, 1, 2, 2>(kvr::AttnParams)", 140.0)
+        put(suffix, 7.0 + 0.05 * sch.hlen_host[s0 + i])
+    put("at::native::spin_kernel(long)", 1.0)
+    put(suffix, 999.0)  # after it
+    c.executemany("insert into kernels values (?, ?, ?, ?)", rows)
+    c.commit()
+    c.close()
+    line = {"steps": K, "config": {"workload": "helper4k", "window": {"first_step": s0, "steps": K}}}
+    bj = tmp_path / "bench.json"
+    bj.write_text("log line\n" + json.dumps(line) + "\n")
+    out = profsum.suffix_fit(str(db), str(bj))
+    m = re.search(r"duration = ([\d.]+) us \+ ([\d.]+) us x u", out[0])
+    assert m and abs(float(m.group(1)) - 7.0) < 0.05 and abs(float(m.group(2)) - 0.05) < 1e-4, out
