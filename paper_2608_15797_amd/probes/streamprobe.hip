@@ -34,6 +34,9 @@
 //       span  the context kernel's split: one 64-lane wave per equal
 //             contiguous span, 1 KiB per load instruction, U in flight, for
 //             several wave counts (1024 = one wave per SIMD, as the kernel).
+//   streamprobe readpol MB [MB ...]
+//     The span pattern through range-checked buffer loads under each cache
+//     policy of the load instruction (default, nt, sc0, sc0 nt, sc1, sc1 nt).
 //
 // Bytes are algorithmic: attention N rows x 512 bytes per unit; eviction the
 // moved rows x 512 bytes, read and written.
@@ -269,6 +272,25 @@ __global__ __launch_bounds__(64) void span_read(const u32x4 *src, size_t n16, si
   out[(size_t)blockIdx.x * 64 + threadIdx.x] = a;
 }
 
+// The span pattern through buffer loads with cache-policy operand AUX (bit 0
+// sc0, bit 1 nt, bit 4 sc1): one resource per wave over its span, so every
+// load is range-checked.
+template <int U, int AUX>
+__global__ __launch_bounds__(64) void span_read_pol(const u32x4 *src, size_t n16, size_t span16, uint32_t *out) {
+  const size_t s0 = (size_t)blockIdx.x * span16;
+  const size_t s1 = s0 + span16 < n16 ? s0 + span16 : n16;
+  const uint32_t len = s1 > s0 ? (uint32_t)((s1 - s0) * 16) : 0u;
+  const rsrc_t r = mk(src + (s1 > s0 ? s0 : 0), len);
+  uint32_t a = 0;
+  for (uint32_t off = threadIdx.x * 16u; off < len; off += U * 1024u) {
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) v[u] = __builtin_amdgcn_raw_buffer_load_b128(r, off + u * 1024u, 0, AUX);
+    a ^= fold(v, U);
+  }
+  out[(size_t)blockIdx.x * 64 + threadIdx.x] = a;
+}
+
 template <typename F>
 static double time_us(F f, int reps = 20) {
   hipEvent_t a, b;
@@ -420,6 +442,49 @@ static int run_read(const std::vector<double> &mbs) {
   return 0;
 }
 
+// Span reads of MB megabytes under each cache policy of the loads.
+static int run_readpol(const std::vector<double> &mbs) {
+  double mx = 0;
+  for (double m : mbs) {
+    if (!(m >= 1.0 && m <= 64000.0)) { printf("MB=%g outside 1..64000\n", m); return 1; }
+    mx = m > mx ? m : mx;
+  }
+  const size_t cap16 = (size_t)(mx * 1e6) / 16;
+  u32x4 *src;
+  uint32_t *out;
+  CK(hipMalloc(&src, cap16 * 16));
+  CK(hipMalloc(&out, (size_t)4096 * 64 * 4));
+  CK(hipMemset(src, 1, cap16 * 16));
+  const char *names[] = {"default", "nt", "sc0", "sc0 nt", "sc1", "sc1 nt"};
+  for (double m : mbs) {
+    const size_t n16 = (size_t)(m * 1e6) / 16;
+    const double b = (double)n16 * 16;
+    for (int w : {1024, 2048, 4096}) {
+      const size_t span16 = (n16 + w - 1) / w;
+      if (span16 * 16 >= (1ull << 31)) { printf("span of %zu bytes exceeds a buffer resource\n", span16 * 16); return 1; }
+      for (int pol = 0; pol < 6; pol++) {
+        double us = time_us([&] {
+          const dim3 g(w), t(64);
+          switch (pol) {
+            case 0: hipLaunchKernelGGL((span_read_pol<8, 0>), g, t, 0, 0, src, n16, span16, out); break;
+            case 1: hipLaunchKernelGGL((span_read_pol<8, 2>), g, t, 0, 0, src, n16, span16, out); break;
+            case 2: hipLaunchKernelGGL((span_read_pol<8, 1>), g, t, 0, 0, src, n16, span16, out); break;
+            case 3: hipLaunchKernelGGL((span_read_pol<8, 3>), g, t, 0, 0, src, n16, span16, out); break;
+            case 4: hipLaunchKernelGGL((span_read_pol<8, 16>), g, t, 0, 0, src, n16, span16, out); break;
+            default: hipLaunchKernelGGL((span_read_pol<8, 18>), g, t, 0, 0, src, n16, span16, out); break;
+          }
+        });
+        printf("readpol %.0f MB span waves=%d U=8 policy=%-8s %9.1f us %6.2f TB/s\n", m, w, names[pol], us,
+               b / (us * 1e-6) / 1e12);
+        fflush(stdout);
+      }
+    }
+  }
+  CK(hipFree(src));
+  CK(hipFree(out));
+  return 0;
+}
+
 int main(int argc, char **argv) {
   if (argc >= 5 && !strcmp(argv[1], "attn")) {
     std::vector<int> ns;
@@ -433,6 +498,12 @@ int main(int argc, char **argv) {
     for (int i = 2; i < argc; i++) mbs.push_back(atof(argv[i]));
     return run_read(mbs);
   }
-  printf("usage: streamprobe attn UNITS CAP N [N ...] | streamprobe evict HEADS CAP B W N | streamprobe read MB [MB ...]\n");
+  if (argc >= 3 && !strcmp(argv[1], "readpol")) {
+    std::vector<double> mbs;
+    for (int i = 2; i < argc; i++) mbs.push_back(atof(argv[i]));
+    return run_readpol(mbs);
+  }
+  printf("usage: streamprobe attn UNITS CAP N [N ...] | streamprobe evict HEADS CAP B W N | streamprobe read MB [MB ...]"
+         " | streamprobe readpol MB [MB ...]\n");
   return 2;
 }
