@@ -437,17 +437,33 @@ __global__ __launch_bounds__(NW * 64) void window_scores_tiled(ScoreParams p) {
       float4_t cc[KRB];
       logits_tile_n<D, KRB>(qa, kv, cc);
       const int j = key0 + col;
+      float x[KRB][4];
+      bool up = false;
 #pragma unroll
       for (int b = 0; b < KRB; b++)
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-          const float x = j < nr[b][i] ? cc[b][i] * c : kNegInf;
-          if (x > m[b][i] + kSlack) {
-            z[b][i] = z[b][i] > 0.f ? z[b][i] * fast_exp2(m[b][i] - x) : 0.f;
-            m[b][i] = x;
-          }
-          z[b][i] += fast_exp2(fmaxf(x - m[b][i], -256.0f));
+          x[b][i] = j < nr[b][i] ? cc[b][i] * c : kNegInf;
+          up |= x[b][i] > m[b][i] + kSlack;
         }
+      // The reference moves on the wave's first keys and then rarely: test
+      // it for the whole wave, so that the rescale (an exp of its own, which
+      // the compiler otherwise issues under a lane mask for every key) is
+      // skipped by a uniform branch.
+      if (__builtin_amdgcn_ballot_w64(up) != 0) {
+#pragma unroll
+        for (int b = 0; b < KRB; b++)
+#pragma unroll
+          for (int i = 0; i < 4; i++)
+            if (x[b][i] > m[b][i] + kSlack) {
+              z[b][i] = z[b][i] > 0.f ? z[b][i] * fast_exp2(m[b][i] - x[b][i]) : 0.f;
+              m[b][i] = x[b][i];
+            }
+      }
+#pragma unroll
+      for (int b = 0; b < KRB; b++)
+#pragma unroll
+        for (int i = 0; i < 4; i++) z[b][i] += fast_exp2(fmaxf(x[b][i] - m[b][i], -256.0f));
     });
     // Merge the 16 lanes that hold the same rows (lane bits 0..3).
 #pragma unroll
