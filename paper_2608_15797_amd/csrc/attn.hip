@@ -34,6 +34,12 @@
 // (candidate, layer, KV head) and folds those partials in by log-sum-exp.
 //
 // f32 path: plain VALU kernel (one wave per unit) for float32 caches.
+//
+// This file is compiled twice. With KVR_ATTN_WIDE = 1 (attn_wide.hip) it
+// provides only the context kernels of three and four row blocks
+// (launch_prefix_wide, prefix_slots_wide), built with the matrix-core
+// accumulators in vector registers; every other kernel and entry point comes
+// from the KVR_ATTN_WIDE = 0 build.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -43,6 +49,9 @@
 #include "kvr_device.h"
 #include "kvr_internal.h"
 
+#ifndef KVR_ATTN_WIDE
+#define KVR_ATTN_WIDE 0
+#endif
 
 namespace kvr {
 
@@ -1028,6 +1037,7 @@ __global__ __launch_bounds__(64) void attn_prefix_rows_bf16(AttnParams p, Entrop
   prefix_wave<D, RB, TILES, DEPTH>(p, blockIdx.x - rows, deferred);
 }
 
+#if !KVR_ATTN_WIDE
 // ---------------------------------------------------------------------------
 // float32 path: one wave per (sequence, layer, KV head), VALU arithmetic.
 // LDS: q rows [G][D], logits [G][nt_max], stats [2][16].
@@ -1119,6 +1129,7 @@ __global__ __launch_bounds__(64) void attn_f32(AttnParams p, int nt_max) {
     }
   }
 }
+#endif  // !KVR_ATTN_WIDE
 
 // LDS of a context-kernel wave: the deferred records of RB * 16 rows. A
 // logit-row wave of the same launch uses the first kSampleRowLds bytes of it.
@@ -1196,8 +1207,8 @@ hipError_t launch_bf16(const AttnParams &p_in, const EntropyBatch *ent, hipStrea
   switch ((p.C * p.G + 15) / 16) {
     case 1: launch_prefix<D, 1, 2>(p, ent, stream); break;
     case 2: launch_prefix<D, 2, 2>(p, ent, stream); break;
-    case 3: launch_prefix<D, 3, 1>(p, ent, stream); break;
-    case 4: launch_prefix<D, 4, 1>(p, ent, stream); break;
+    case 3: launch_prefix_wide(D, 3, p, ent, stream); break;
+    case 4: launch_prefix_wide(D, 4, p, ent, stream); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
@@ -1227,9 +1238,11 @@ __global__ __launch_bounds__(64) void entropy_rows_kernel(EntropyBatch e) {
 
 }  // namespace
 
+#if !KVR_ATTN_WIDE
 size_t f32_attn_lds_bytes(int G, int D, int plen, int cap) {
   return ((size_t)G * D + (size_t)G * (plen + cap) + 32) * sizeof(float);
 }
+#endif
 
 namespace {
 
@@ -1258,13 +1271,13 @@ int prefix_slots() {
   return v;
 }
 
+#if !KVR_ATTN_WIDE
 template <int D, bool ROWS>
 int prefix_slots_for(int rb) {
   switch (rb) {
     case 1: return prefix_slots<D, 1, 2, ROWS>();
     case 2: return prefix_slots<D, 2, 2, ROWS>();
-    case 3: return prefix_slots<D, 3, 1, ROWS>();
-    default: return prefix_slots<D, 4, 1, ROWS>();
+    default: return (int)prefix_slots_wide(D, rb, ROWS);
   }
 }
 
@@ -1272,8 +1285,11 @@ long slots_for(int D, int rb, bool rows) {
   if (D == 128) return rows ? prefix_slots_for<128, true>(rb) : prefix_slots_for<128, false>(rb);
   return rows ? prefix_slots_for<64, true>(rb) : prefix_slots_for<64, false>(rb);
 }
+#endif  // !KVR_ATTN_WIDE
 
 }  // namespace
+
+#if !KVR_ATTN_WIDE
 
 void plan_prefix_splits(int D, int P, int L, int Hkv, int plen, int rows, int ent_rows, int *nsplit, int *span,
                         int *nwaves) {
@@ -1327,5 +1343,28 @@ hipError_t launch_decode_attn(const AttnParams &p, const EntropyBatch *ent, hipS
   }
   return p.D == 128 ? launch_bf16<128>(p, ent, stream) : launch_bf16<64>(p, ent, stream);
 }
+
+#else  // KVR_ATTN_WIDE
+
+void launch_prefix_wide(int D, int rb, const AttnParams &p, const EntropyBatch *e, hipStream_t stream) {
+  if (D == 128) {
+    if (rb == 3) launch_prefix<128, 3, 1>(p, e, stream);
+    else launch_prefix<128, 4, 1>(p, e, stream);
+  } else {
+    if (rb == 3) launch_prefix<64, 3, 1>(p, e, stream);
+    else launch_prefix<64, 4, 1>(p, e, stream);
+  }
+}
+
+long prefix_slots_wide(int D, int rb, bool rows) {
+  if (D == 128) {
+    if (rb == 3) return rows ? prefix_slots<128, 3, 1, true>() : prefix_slots<128, 3, 1, false>();
+    return rows ? prefix_slots<128, 4, 1, true>() : prefix_slots<128, 4, 1, false>();
+  }
+  if (rb == 3) return rows ? prefix_slots<64, 3, 1, true>() : prefix_slots<64, 3, 1, false>();
+  return rows ? prefix_slots<64, 4, 1, true>() : prefix_slots<64, 4, 1, false>();
+}
+
+#endif  // KVR_ATTN_WIDE
 
 }  // namespace kvr

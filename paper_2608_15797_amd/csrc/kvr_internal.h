@@ -50,6 +50,11 @@ struct EntropyBatch;
 // ent: NULL, or the entropy rows computed in the same launch (rows 16-byte
 // aligned, no workspace): with the own-cache kernel, or with a prefix in the
 // context kernel (p planned with ent_rows = the batch's rows).
+// Context kernels of three and four row blocks (rb = 3 or 4), built in a
+// translation unit of their own with the matrix-core accumulators in vector
+// registers: the launch, and the waves of it the chip holds at once.
+void launch_prefix_wide(int D, int rb, const AttnParams &p, const EntropyBatch *e, hipStream_t stream);
+long prefix_slots_wide(int D, int rb, bool rows);
 hipError_t launch_decode_attn(const AttnParams &p, const EntropyBatch *ent, hipStream_t stream);
 
 struct ScoreParams {

@@ -41,8 +41,8 @@ CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 CALL_SOURCES = {
     "base_attn": ("attn.hip", "kvr_device.h"),
     "base_attn_entropy": ("attn.hip", "entropy_common.h", "sampler_common.h", "kvr_device.h"),
-    "helper_attn": ("attn.hip", "kvr_device.h"),
-    "helper_attn_entropy": ("attn.hip", "entropy_common.h", "sampler_common.h", "kvr_device.h"),
+    "helper_attn": ("attn.hip", "attn_wide.hip", "kvr_device.h"),
+    "helper_attn_entropy": ("attn.hip", "attn_wide.hip", "entropy_common.h", "sampler_common.h", "kvr_device.h"),
     "evict": ("evict.hip", "kvr_device.h"),
     "entropy": ("entropy.hip", "entropy_common.h", "kvr_device.h"),
 }
