@@ -197,6 +197,8 @@ def counters(db: str, window=None) -> dict:
         return agg
     order = _pick(cols, "dispatch_id", "correlation_id")
     rows = [dict(zip(cols, row)) for row in c.execute("select * from counters_collection")]
+    if not rows:  # a kernel trace: the view exists, empty
+        return agg
     bounds = None
     if window is not None:
         if order is None:
