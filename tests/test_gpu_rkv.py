@@ -40,6 +40,12 @@ CASES = [
     (3, 1, 2, 128, 20, 4, 12, torch.float32, 0.1, 7),
     (2, 1, 3, 64, 16, 8, 16, torch.float32, 1.0, 1),
     (2, 1, 1, 128, 64, 16, 64, torch.bfloat16, 0.0, 7),
+    # Heads longer than the keys a lane keeps in registers between the two
+    # passes (256 candidates of a float32 D = 128 head, 1024 of a bf16 D = 64
+    # head, 512 of a bf16 D = 128 head): the rest is read twice.
+    (2, 1, 2, 128, 600, 16, 100, torch.float32, 0.1, 7),
+    (2, 1, 2, 64, 1100, 32, 100, torch.bfloat16, 0.1, 5),
+    (1, 1, 2, 128, 900, 64, 200, torch.bfloat16, 0.3, 7),
 ]
 
 
