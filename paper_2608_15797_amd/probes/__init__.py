@@ -5,11 +5,13 @@
     python -m paper_2608_15797_amd.probes stream evict HEADS CAP B W N
     python -m paper_2608_15797_amd.probes stream read MB [MB ...]
     python -m paper_2608_15797_amd.probes stream readpol MB [MB ...]
+    python -m paper_2608_15797_amd.probes stream lanes
     python -m paper_2608_15797_amd.probes entropy [--rows 0,1,8,32,64,128,256]
 
 `stream` builds and runs streamprobe.hip (load-only attention streams,
 eviction-shaped copies, plain read-only streams and the same streams under
-each cache policy of the loads; see that file). `entropy` times the library's
+each cache policy of the loads, and the lane layout of the cross-lane swap
+instructions; see that file). `entropy` times the library's
 base-attention launch with and without the step's entropy rows in it
 (kvr_decode_attn_entropy against kvr_decode_attn), at fixed cache lengths of
 the 72B and 7B B=128 base shapes, for several numbers of 152064-logit rows:

@@ -71,7 +71,7 @@ def entropy_marginal(rows):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__)
     sub = ap.add_subparsers(dest="cmd", required=True)
-    st = sub.add_parser("stream", help="run streamprobe (attn ... | evict ... | read ... | readpol ...)")
+    st = sub.add_parser("stream", help="run streamprobe (attn ... | evict ... | read ... | readpol ... | lanes)")
     st.add_argument("args", nargs=argparse.REMAINDER)
     en = sub.add_parser("entropy", help="entropy's marginal time in the fused base-attention launch")
     en.add_argument("--rows", default="0,1,8,32,64,128,256")

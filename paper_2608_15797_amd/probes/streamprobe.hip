@@ -485,6 +485,39 @@ static int run_readpol(const std::vector<double> &mbs) {
   return 0;
 }
 
+// Lane layout of the gfx950 lane swaps between 16-lane rows and between
+// 32-lane halves: one wave, x = lane id; each lane writes the two results of
+// each swap (64 x 4 words). A swap that leaves {l, l^16} (or {l, l^32}) in a
+// lane's two results makes their max or sum the xor-16 (xor-32) reduction.
+__global__ __launch_bounds__(64) void lane_swap_probe(unsigned *out) {
+  const unsigned x = threadIdx.x;
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  const auto b = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  out[threadIdx.x * 4 + 0] = a[0];
+  out[threadIdx.x * 4 + 1] = a[1];
+  out[threadIdx.x * 4 + 2] = b[0];
+  out[threadIdx.x * 4 + 3] = b[1];
+}
+
+static int run_lanes() {
+  unsigned *d = nullptr, h[256];
+  CK(hipMalloc(&d, sizeof(h)));
+  hipLaunchKernelGGL(lane_swap_probe, dim3(1), dim3(64), 0, 0, d);
+  CK(hipGetLastError());
+  CK(hipMemcpy(h, d, sizeof(h), hipMemcpyDeviceToHost));
+  CK(hipFree(d));
+  bool ok16 = true, ok32 = true;
+  for (unsigned l = 0; l < 64; l++) {
+    const unsigned p0 = h[4 * l], p1 = h[4 * l + 1], q0 = h[4 * l + 2], q1 = h[4 * l + 3];
+    ok16 = ok16 && ((p0 == l && p1 == (l ^ 16)) || (p1 == l && p0 == (l ^ 16)));
+    ok32 = ok32 && ((q0 == l && q1 == (l ^ 32)) || (q1 == l && q0 == (l ^ 32)));
+    if (l % 8 == 0) printf("lane %2u: swap16 %2u %2u  swap32 %2u %2u\n", l, p0, p1, q0, q1);
+  }
+  printf("swap16 pairs lane l with l^16: %s\nswap32 pairs lane l with l^32: %s\n", ok16 ? "yes" : "no",
+         ok32 ? "yes" : "no");
+  return ok16 && ok32 ? 0 : 1;
+}
+
 int main(int argc, char **argv) {
   if (argc >= 5 && !strcmp(argv[1], "attn")) {
     std::vector<int> ns;
@@ -503,7 +536,8 @@ int main(int argc, char **argv) {
     for (int i = 2; i < argc; i++) mbs.push_back(atof(argv[i]));
     return run_readpol(mbs);
   }
+  if (argc == 2 && !strcmp(argv[1], "lanes")) return run_lanes();
   printf("usage: streamprobe attn UNITS CAP N [N ...] | streamprobe evict HEADS CAP B W N | streamprobe read MB [MB ...]"
-         " | streamprobe readpol MB [MB ...]\n");
+         " | streamprobe readpol MB [MB ...] | streamprobe lanes\n");
   return 2;
 }
